@@ -1,0 +1,77 @@
+// Internal launch interface of the HIP kernels (not part of the C ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+namespace kvp {
+
+// B operand of the projection GEMMs: up to three row blocks [rows_i][K]
+// stacked along N (W_Q; W_K; W_V), each a separate caller buffer.
+struct WRows {
+    const void* p[3];
+    int rows[3];
+};
+
+// ---- bf16 prefill ---------------------------------------------------------
+
+// Q (all layers) and K, V (producers) projections with RoPE fused into the
+// epilogue.  x [M = B*S][K]; writes q [M][n_q] (post-RoPE), K slot rows
+// (post-RoPE) and transposed V slot rows at positions s = m % S.
+struct QkvOut {
+    uint16_t* q;          // [M][n_q]
+    uint16_t* kc;         // K slot [Bmax][g][cap][128] or nullptr
+    uint16_t* vc;         // V slot [Bmax][g][128][cap] or nullptr
+    const float2* rope;   // [S][64] (cos, sin)
+    int n_q, n_kv, g, cap, S;
+};
+hipError_t gemm_qkv_bf16(const uint16_t* x, const WRows& w, int M, int N, int K, const QkvOut& o,
+                         hipStream_t st);
+
+// y = x_res + a @ w^T, a [M][K], w [N][K], x_res, y [M][N].
+hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const uint16_t* x_res,
+                           uint16_t* y, int M, int N, int K, hipStream_t st);
+
+// Causal flash attention: q [B*S][a*128], K/V slots of the producer, o [B*S][a*128].
+hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                              uint16_t* o, int B, int S, int a, int g, int cap, hipStream_t st);
+
+// ---- bf16 decode ------------------------------------------------------------
+
+// out_f32 [M][N] = x @ w^T (M <= 64), or (resid) y = x_res + x @ w^T in bf16.
+hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
+                            float* out_f32, const uint16_t* x_res, uint16_t* y, hipStream_t st);
+
+// Split-K attention of one new query per sequence over positions [0, len_b].
+hipError_t decode_attn_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
+                            const int32_t* lens, float* part, int B, int a, int g, int cap,
+                            int split, int nsplit, hipStream_t st);
+hipError_t decode_combine_bf16(const float* part, const int32_t* lens, uint16_t* o, int B, int a,
+                               int cap, int split, int nsplit, hipStream_t st);
+
+// ---- shared by both dtypes -------------------------------------------------
+
+// table[pos][i] = (cos, sin)(pos * base^(-2i/d)), evaluated in double.
+hipError_t rope_table(float2* table, int S, int d, double base, hipStream_t st);
+
+// RoPE + scatter of fp32 projections proj [rows][n_q + 2*n_kv]:
+// Q -> q [rows][n_q], K -> K slot, V -> V slot (transposed).  Row r is
+// sequence r / S at position r % S (lens == nullptr), or sequence r at
+// position lens[r].
+hipError_t rope_scatter(const float* proj, int rows, int S, const int32_t* lens, int a, int g,
+                        int d, int cap, double base, bool producer, bool bf16, void* q, void* kc,
+                        void* vc, hipStream_t st);
+
+// ---- fp32 model path (vector ALU, full fp32) -------------------------------
+
+// out [M][N] = a @ w^T (fp32), or y = x_res + a @ w^T when x_res != nullptr.
+hipError_t gemm_f32(const float* a, const WRows& w, int M, int N, int K, float* out,
+                    const float* x_res, hipStream_t st);
+
+// Attention for fp32 models: row r of q [rows][a*d] is sequence r / S at
+// position r % S (lens == nullptr) or sequence r at lens[r]; attends [0, pos].
+hipError_t attn_f32(const float* q, const float* kc, const float* vc, const int32_t* lens,
+                    float* o, int rows, int S, int a, int g, int d, int cap, hipStream_t st);
+
+}  // namespace kvp

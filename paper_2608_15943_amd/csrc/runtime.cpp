@@ -1,0 +1,569 @@
+// Host runtime behind the C ABI: context, validation, workspace layout and the
+// sharing-map-driven layer scheduler.
+//
+// For every layer l the scheduler looks up its producer p = tau(l) (Eq. 3):
+//   producer (p == l): fused Q|K|V projection (K, V written into slot l, RoPE
+//                      fused) -> attention on slot l -> O projection + residual;
+//   consumer (p <  l): Q-only projection -> attention on slot p -> O projection
+//                      + residual.
+// All launches go to the caller's stream in layer order; the library allocates
+// no device memory and keeps only host-side state.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdint>
+#include <cstring>
+#include <vector>
+
+#include "kernels.h"
+#include "kvpipe.h"
+#include "status.h"
+
+namespace kvp {
+
+char* last_error_buffer() {
+    static thread_local char buf[512];
+    return buf;
+}
+
+}  // namespace kvp
+
+using kvp::fail;
+using kvp::ok;
+
+namespace {
+
+struct Layer {
+    const void* wq = nullptr;
+    const void* wk = nullptr;
+    const void* wv = nullptr;
+    const void* wo = nullptr;
+    void* kc = nullptr;
+    void* vc = nullptr;
+    bool weights = false;
+};
+
+constexpr size_t kAlign = 256;
+constexpr int kMinSplit = 256;       // smallest decode split (positions per wave)
+constexpr int kDecodeMaxRows = 64;   // rows of the skinny decode GEMM
+constexpr int kTargetWaves = 4096;   // decode: split-K waves per layer to aim for
+
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+struct Workspace {
+    size_t q = 0, o = 0, x = 0, rope = 0, proj = 0, part = 0, total = 0;
+};
+
+}  // namespace
+
+struct kvp_ctx {
+    struct ProfRec {
+        int kind;
+        hipEvent_t start, stop;
+    };
+    kvp_model_desc d;
+    std::vector<int32_t> tau;
+    std::vector<Layer> layers;
+    bool prof = false;
+    std::vector<ProfRec> recs;        // launches timed since the last read
+    std::vector<hipEvent_t> pool;     // idle events for reuse
+    ~kvp_ctx() {
+        for (auto& r : recs) {
+            hipEventDestroy(r.start);
+            hipEventDestroy(r.stop);
+        }
+        for (auto e : pool) hipEventDestroy(e);
+    }
+    bool bf16() const { return d.dtype == KVP_DTYPE_BF16; }
+    size_t esize() const { return bf16() ? 2 : 4; }
+    int n_q() const { return d.a * d.d_h; }
+    int n_kv() const { return d.g * d.d_h; }
+};
+
+namespace {
+
+Workspace layout(const kvp_ctx& c, int phase, int B, int S) {
+    Workspace w;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align_up(bytes);
+        return at;
+    };
+    const size_t e = c.esize();
+    const size_t rows = phase == KVP_PHASE_PREFILL ? (size_t)B * S : (size_t)B;
+    const size_t nproj = (size_t)(c.d.a + 2 * c.d.g) * c.d.d_h;
+    w.q = take(rows * c.n_q() * e);
+    w.o = take(rows * c.n_q() * e);
+    w.x = take(rows * c.d.h * e);
+    if (phase == KVP_PHASE_PREFILL) {
+        if (c.bf16())
+            w.rope = take((size_t)S * (c.d.d_h / 2) * sizeof(float2));
+        else
+            w.proj = take(rows * nproj * sizeof(float));
+    } else {
+        w.proj = take(rows * nproj * sizeof(float));
+        if (c.bf16()) {
+            const size_t nsplit = (c.d.kv_capacity + kMinSplit - 1) / kMinSplit;
+            w.part = take((size_t)B * c.d.a * nsplit * 132 * sizeof(float));
+        }
+    }
+    w.total = off;
+    return w;
+}
+
+int check_hip(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(KVP_E_HIP, "%s: %s", what, hipGetErrorString(e));
+    return KVP_OK;
+}
+
+hipError_t take_event(kvp_ctx* c, hipEvent_t* e) {
+    if (!c->pool.empty()) {
+        *e = c->pool.back();
+        c->pool.pop_back();
+        return hipSuccess;
+    }
+    return hipEventCreate(e);
+}
+
+// Runs launch(); when timing is on, brackets it with two events on st.
+template <class F>
+int timed(kvp_ctx* c, int kind, hipStream_t st, F&& launch) {
+    if (!c->prof) return launch();
+    hipEvent_t a, b;
+    int rc;
+    if ((rc = check_hip(take_event(c, &a), "hipEventCreate"))) return rc;
+    if ((rc = check_hip(take_event(c, &b), "hipEventCreate"))) {
+        c->pool.push_back(a);
+        return rc;
+    }
+    if ((rc = check_hip(hipEventRecord(a, st), "hipEventRecord"))) return rc;
+    rc = launch();
+    const int rc2 = check_hip(hipEventRecord(b, st), "hipEventRecord");
+    c->recs.push_back({kind, a, b});
+    return rc ? rc : rc2;
+}
+
+int check_layers(const kvp_ctx* c, int lo, int hi) {
+    for (int l = lo; l < hi; ++l) {
+        if (!c->layers[l].weights) return fail(KVP_E_STATE, "weights of layer %d were never set", l);
+        const int p = c->tau[l];
+        if (!c->layers[p].kc || !c->layers[p].vc)
+            return fail(KVP_E_STATE, "KV slot of producer %d (used by layer %d) was never set", p, l);
+    }
+    return KVP_OK;
+}
+
+kvp::WRows proj_rows(const kvp_ctx* c, int l, bool producer) {
+    const Layer& L = c->layers[l];
+    kvp::WRows w{};
+    w.p[0] = L.wq;
+    w.rows[0] = c->n_q();
+    if (producer) {
+        w.p[1] = L.wk;
+        w.rows[1] = c->n_kv();
+        w.p[2] = L.wv;
+        w.rows[2] = c->n_kv();
+    }
+    return w;
+}
+
+// One prefill layer: x_in [B*S, h] -> y_out, attention output into o_buf.
+int run_prefill_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, void* o_buf, char* ws,
+                      const Workspace& w, int B, int S, hipStream_t st) {
+    const int p = c->tau[l];
+    const bool producer = p == l;
+    const Layer& P = c->layers[p];
+    const int M = B * S, h = c->d.h, nq = c->n_q();
+    const int N = producer ? nq + 2 * c->n_kv() : nq;
+    const kvp::WRows wr = proj_rows(c, l, producer);
+    kvp::WRows wo{};
+    wo.p[0] = c->layers[l].wo;
+    wo.rows[0] = h;
+    int rc;
+    if (c->bf16()) {
+        kvp::QkvOut qo{};
+        qo.q = (uint16_t*)(ws + w.q);
+        qo.kc = producer ? (uint16_t*)P.kc : nullptr;
+        qo.vc = producer ? (uint16_t*)P.vc : nullptr;
+        qo.rope = (const float2*)(ws + w.rope);
+        qo.n_q = nq;
+        qo.n_kv = producer ? c->n_kv() : 0;
+        qo.g = c->d.g;
+        qo.cap = c->d.kv_capacity;
+        qo.S = S;
+        if ((rc = timed(c, KVP_K_QKV_GEMM, st, [&] {
+                 return check_hip(kvp::gemm_qkv_bf16((const uint16_t*)x_in, wr, M, N, h, qo, st),
+                                  "projection GEMM");
+             })))
+            return rc;
+        if ((rc = timed(c, KVP_K_FLASH_ATTN, st, [&] {
+                 return check_hip(kvp::flash_prefill_bf16(qo.q, (const uint16_t*)P.kc,
+                                                          (const uint16_t*)P.vc, (uint16_t*)o_buf, B,
+                                                          S, c->d.a, c->d.g, c->d.kv_capacity, st),
+                                  "flash attention");
+             })))
+            return rc;
+        return timed(c, KVP_K_OPROJ_GEMM, st, [&] {
+            return check_hip(kvp::gemm_resid_bf16((const uint16_t*)o_buf, (const uint16_t*)wo.p[0],
+                                                  (const uint16_t*)x_in, (uint16_t*)y_out, M, h, nq, st),
+                             "output projection");
+        });
+    }
+    float* proj = (float*)(ws + w.proj);
+    float* q = (float*)(ws + w.q);
+    if ((rc = timed(c, KVP_K_QKV_GEMM, st, [&] {
+             return check_hip(kvp::gemm_f32((const float*)x_in, wr, M, N, h, proj, nullptr, st),
+                              "projection GEMM (fp32)");
+         })))
+        return rc;
+    if ((rc = timed(c, KVP_K_F32_ROPE, st, [&] {
+             return check_hip(kvp::rope_scatter(proj, M, S, nullptr, c->d.a, c->d.g, c->d.d_h,
+                                                c->d.kv_capacity, c->d.rope_base, producer, false, q,
+                                                producer ? P.kc : nullptr, producer ? P.vc : nullptr,
+                                                st),
+                              "RoPE (fp32)");
+         })))
+        return rc;
+    if ((rc = timed(c, KVP_K_F32_ATTN, st, [&] {
+             return check_hip(kvp::attn_f32(q, (const float*)P.kc, (const float*)P.vc, nullptr,
+                                            (float*)o_buf, M, S, c->d.a, c->d.g, c->d.d_h,
+                                            c->d.kv_capacity, st),
+                              "attention (fp32)");
+         })))
+        return rc;
+    return timed(c, KVP_K_OPROJ_GEMM, st, [&] {
+        return check_hip(kvp::gemm_f32((const float*)o_buf, wo, M, h, nq, (float*)y_out,
+                                       (const float*)x_in, st),
+                         "output projection (fp32)");
+    });
+}
+
+int choose_split(const kvp_ctx* c, int B, int max_len, int* nsplit) {
+    const int total = max_len + 1;
+    const int pairs = B * c->d.g;
+    const int want = std::max(1, (kTargetWaves + pairs - 1) / pairs);
+    int split = (total + want - 1) / want;
+    split = std::max(kMinSplit, (split + 63) / 64 * 64);
+    *nsplit = (total + split - 1) / split;
+    return split;
+}
+
+int run_decode_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, const int32_t* lens,
+                     int max_len, char* ws, const Workspace& w, int B, hipStream_t st) {
+    const int p = c->tau[l];
+    const bool producer = p == l;
+    const Layer& P = c->layers[p];
+    const int h = c->d.h, nq = c->n_q();
+    const int N = producer ? nq + 2 * c->n_kv() : nq;
+    const kvp::WRows wr = proj_rows(c, l, producer);
+    kvp::WRows wo{};
+    wo.p[0] = c->layers[l].wo;
+    wo.rows[0] = h;
+    float* proj = (float*)(ws + w.proj);
+    void* q = ws + w.q;
+    void* o = ws + w.o;
+    int rc;
+    if ((rc = timed(c, KVP_K_DEC_GEMM, st, [&] {
+             return c->bf16()
+                        ? check_hip(kvp::gemm_skinny_bf16((const uint16_t*)x_in, wr, B, N, h, proj,
+                                                          nullptr, nullptr, st),
+                                    "decode projection GEMM")
+                        : check_hip(kvp::gemm_f32((const float*)x_in, wr, B, N, h, proj, nullptr, st),
+                                    "decode projection GEMM (fp32)");
+         })))
+        return rc;
+    if ((rc = timed(c, KVP_K_DEC_ROPE, st, [&] {
+             return check_hip(kvp::rope_scatter(proj, B, 0, lens, c->d.a, c->d.g, c->d.d_h,
+                                                c->d.kv_capacity, c->d.rope_base, producer, c->bf16(),
+                                                q, producer ? P.kc : nullptr,
+                                                producer ? P.vc : nullptr, st),
+                              "decode RoPE + cache append");
+         })))
+        return rc;
+    if (c->bf16()) {
+        int nsplit = 0;
+        const int split = choose_split(c, B, max_len, &nsplit);
+        float* part = (float*)(ws + w.part);
+        if ((rc = timed(c, KVP_K_DEC_ATTN, st, [&] {
+                 return check_hip(kvp::decode_attn_bf16((const uint16_t*)q, (const uint16_t*)P.kc,
+                                                        (const uint16_t*)P.vc, lens, part, B, c->d.a,
+                                                        c->d.g, c->d.kv_capacity, split, nsplit, st),
+                                  "decode attention");
+             })))
+            return rc;
+        if ((rc = timed(c, KVP_K_DEC_COMBINE, st, [&] {
+                 return check_hip(kvp::decode_combine_bf16(part, lens, (uint16_t*)o, B, c->d.a,
+                                                           c->d.kv_capacity, split, nsplit, st),
+                                  "decode combine");
+             })))
+            return rc;
+        return timed(c, KVP_K_DEC_OPROJ, st, [&] {
+            return check_hip(kvp::gemm_skinny_bf16((const uint16_t*)o, wo, B, h, nq, nullptr,
+                                                   (const uint16_t*)x_in, (uint16_t*)y_out, st),
+                             "decode output projection");
+        });
+    }
+    if ((rc = timed(c, KVP_K_F32_ATTN, st, [&] {
+             return check_hip(kvp::attn_f32((const float*)q, (const float*)P.kc, (const float*)P.vc,
+                                            lens, (float*)o, B, 0, c->d.a, c->d.g, c->d.d_h,
+                                            c->d.kv_capacity, st),
+                              "decode attention (fp32)");
+         })))
+        return rc;
+    return timed(c, KVP_K_DEC_OPROJ, st, [&] {
+        return check_hip(kvp::gemm_f32((const float*)o, wo, B, h, nq, (float*)y_out, (const float*)x_in,
+                                       st),
+                         "decode output projection (fp32)");
+    });
+}
+
+}  // namespace
+
+// ============================================================================
+// C ABI
+// ============================================================================
+
+extern "C" const char* kvp_status_string(int s) {
+    switch (s) {
+        case KVP_OK: return "KVP_OK";
+        case KVP_E_INVALID_ARG: return "KVP_E_INVALID_ARG";
+        case KVP_E_BAD_MAP: return "KVP_E_BAD_MAP";
+        case KVP_E_SHAPE: return "KVP_E_SHAPE";
+        case KVP_E_WORKSPACE: return "KVP_E_WORKSPACE";
+        case KVP_E_CAPACITY: return "KVP_E_CAPACITY";
+        case KVP_E_HIP: return "KVP_E_HIP";
+        case KVP_E_STATE: return "KVP_E_STATE";
+        default: return "KVP_E_UNKNOWN";
+    }
+}
+
+extern "C" const char* kvp_last_error(void) { return kvp::last_error_buffer(); }
+
+extern "C" int kvp_create(const kvp_model_desc* desc, const int32_t* tau, kvp_ctx** out) {
+    if (!out) return fail(KVP_E_INVALID_ARG, "kvp_create: out is NULL");
+    *out = nullptr;
+    if (!desc || !tau) return fail(KVP_E_INVALID_ARG, "kvp_create: NULL desc or tau");
+    const kvp_model_desc& d = *desc;
+    if (d.L < 1 || d.h < 1 || d.a < 1 || d.g < 1 || d.d_h < 2 || d.max_batch < 1 || d.max_seq < 1 ||
+        d.kv_capacity < 1)
+        return fail(KVP_E_INVALID_ARG, "kvp_create: sizes must be positive");
+    if (!(d.rope_base > 0.0)) return fail(KVP_E_INVALID_ARG, "kvp_create: rope_base must be > 0");
+    if (d.dtype != KVP_DTYPE_BF16 && d.dtype != KVP_DTYPE_FP32)
+        return fail(KVP_E_INVALID_ARG, "kvp_create: unknown dtype %d", d.dtype);
+    if (d.a % d.g) return fail(KVP_E_INVALID_ARG, "kvp_create: g must divide a");
+    if ((int64_t)d.a * d.d_h != d.h) return fail(KVP_E_INVALID_ARG, "kvp_create: need a * d_h == h");
+    if (d.max_seq > d.kv_capacity)
+        return fail(KVP_E_INVALID_ARG, "kvp_create: max_seq exceeds kv_capacity");
+    if (d.dtype == KVP_DTYPE_BF16) {
+        if (d.d_h != 128) return fail(KVP_E_SHAPE, "kvp_create: bf16 models need d_h == 128");
+        if (d.kv_capacity % 64)
+            return fail(KVP_E_SHAPE, "kvp_create: bf16 models need kv_capacity % 64 == 0");
+        if (d.a / d.g > 16) return fail(KVP_E_SHAPE, "kvp_create: bf16 decode supports a / g <= 16");
+    } else if (d.d_h != 16 && d.d_h != 32 && d.d_h != 64 && d.d_h != 128) {
+        return fail(KVP_E_SHAPE, "kvp_create: fp32 models need d_h in {16, 32, 64, 128}");
+    }
+    std::vector<int32_t> canon(d.L);
+    const int rc = kvp_canonicalize_map(d.L, tau, canon.data());
+    if (rc) return rc;
+    kvp_ctx* c = new (std::nothrow) kvp_ctx;
+    if (!c) return fail(KVP_E_INVALID_ARG, "kvp_create: out of host memory");
+    c->d = d;
+    c->tau = std::move(canon);
+    c->layers.resize(d.L);
+    *out = c;
+    return ok();
+}
+
+extern "C" int kvp_destroy(kvp_ctx* ctx) {
+    delete ctx;
+    return ok();
+}
+
+extern "C" int kvp_profile_enable(kvp_ctx* ctx, int enable) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "kvp_profile_enable: NULL ctx");
+    for (auto& r : ctx->recs) {
+        ctx->pool.push_back(r.start);
+        ctx->pool.push_back(r.stop);
+    }
+    ctx->recs.clear();
+    ctx->prof = enable != 0;
+    return ok();
+}
+
+extern "C" int kvp_profile_read(kvp_ctx* ctx, double* ms, int64_t* launches) {
+    if (!ctx || !ms || !launches) return fail(KVP_E_INVALID_ARG, "kvp_profile_read: NULL argument");
+    for (int k = 0; k < KVP_NUM_KERNEL_KINDS; ++k) {
+        ms[k] = 0.0;
+        launches[k] = 0;
+    }
+    int rc = KVP_OK;
+    for (auto& r : ctx->recs) {
+        float t = 0.f;
+        if (!rc) rc = check_hip(hipEventSynchronize(r.stop), "hipEventSynchronize");
+        if (!rc) rc = check_hip(hipEventElapsedTime(&t, r.start, r.stop), "hipEventElapsedTime");
+        if (!rc && r.kind >= 0 && r.kind < KVP_NUM_KERNEL_KINDS) {
+            ms[r.kind] += t;
+            launches[r.kind] += 1;
+        }
+        ctx->pool.push_back(r.start);
+        ctx->pool.push_back(r.stop);
+    }
+    ctx->recs.clear();
+    return rc;
+}
+
+extern "C" int kvp_get_map(const kvp_ctx* ctx, int32_t* tau) {
+    if (!ctx || !tau) return fail(KVP_E_INVALID_ARG, "kvp_get_map: NULL argument");
+    std::memcpy(tau, ctx->tau.data(), sizeof(int32_t) * ctx->d.L);
+    return ok();
+}
+
+extern "C" int kvp_set_layer(kvp_ctx* ctx, int l, const void* Wq, const void* Wk, const void* Wv,
+                             const void* Wo) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "kvp_set_layer: NULL ctx");
+    if (l < 0 || l >= ctx->d.L) return fail(KVP_E_INVALID_ARG, "kvp_set_layer: layer %d out of range", l);
+    const bool producer = ctx->tau[l] == l;
+    if (!Wq || !Wo) return fail(KVP_E_INVALID_ARG, "kvp_set_layer: Wq and Wo are required");
+    if (producer && (!Wk || !Wv))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_layer: layer %d is a producer and needs Wk, Wv", l);
+    if (!producer && (Wk || Wv))
+        return fail(KVP_E_INVALID_ARG,
+                    "kvp_set_layer: layer %d shares K/V of layer %d and takes no Wk, Wv", l,
+                    ctx->tau[l]);
+    if (!aligned16(Wq) || !aligned16(Wo) || (Wk && !aligned16(Wk)) || (Wv && !aligned16(Wv)))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_layer: weights must be 16-byte aligned");
+    Layer& L = ctx->layers[l];
+    L.wq = Wq;
+    L.wk = Wk;
+    L.wv = Wv;
+    L.wo = Wo;
+    L.weights = true;
+    return ok();
+}
+
+extern "C" int kvp_set_kv_slot(kvp_ctx* ctx, int l, void* K, void* V) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "kvp_set_kv_slot: NULL ctx");
+    if (l < 0 || l >= ctx->d.L) return fail(KVP_E_INVALID_ARG, "kvp_set_kv_slot: layer %d out of range", l);
+    if (ctx->tau[l] != l)
+        return fail(KVP_E_INVALID_ARG, "kvp_set_kv_slot: layer %d is a consumer and owns no slot", l);
+    if (!K || !V) return fail(KVP_E_INVALID_ARG, "kvp_set_kv_slot: NULL K or V");
+    if (!aligned16(K) || !aligned16(V))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_kv_slot: slots must be 16-byte aligned");
+    ctx->layers[l].kc = K;
+    ctx->layers[l].vc = V;
+    return ok();
+}
+
+extern "C" int kvp_workspace_size(const kvp_ctx* ctx, int phase, int B, int S, size_t* bytes) {
+    if (!ctx || !bytes) return fail(KVP_E_INVALID_ARG, "kvp_workspace_size: NULL argument");
+    if (phase != KVP_PHASE_PREFILL && phase != KVP_PHASE_DECODE)
+        return fail(KVP_E_INVALID_ARG, "kvp_workspace_size: unknown phase");
+    if (B < 1 || (phase == KVP_PHASE_PREFILL && S < 1))
+        return fail(KVP_E_INVALID_ARG, "kvp_workspace_size: B and S must be >= 1");
+    if (B > ctx->d.max_batch) return fail(KVP_E_CAPACITY, "kvp_workspace_size: B > max_batch");
+    if (phase == KVP_PHASE_PREFILL && S > ctx->d.max_seq)
+        return fail(KVP_E_CAPACITY, "kvp_workspace_size: S > max_seq");
+    *bytes = layout(*ctx, phase, B, phase == KVP_PHASE_PREFILL ? S : 1).total;
+    return ok();
+}
+
+namespace {
+
+int check_prefill_args(const kvp_ctx* ctx, const void* x, const void* y, int B, int S, void* ws,
+                       size_t ws_bytes, Workspace* w) {
+    if (!ctx || !x || !y) return fail(KVP_E_INVALID_ARG, "prefill: NULL ctx, x or y");
+    if (x == y) return fail(KVP_E_INVALID_ARG, "prefill: x and y must not alias");
+    if (!aligned16(x) || !aligned16(y)) return fail(KVP_E_INVALID_ARG, "prefill: x, y must be 16-byte aligned");
+    if (B < 1 || S < 1) return fail(KVP_E_INVALID_ARG, "prefill: B and S must be >= 1");
+    if (B > ctx->d.max_batch || S > ctx->d.max_seq)
+        return fail(KVP_E_CAPACITY, "prefill: B=%d, S=%d exceed max_batch=%d / max_seq=%d", B, S,
+                    ctx->d.max_batch, ctx->d.max_seq);
+    if ((int64_t)B * S > INT32_MAX / std::max(ctx->d.h, 1))
+        return fail(KVP_E_SHAPE, "prefill: B * S * h exceeds the 32-bit row index range");
+    *w = layout(*ctx, KVP_PHASE_PREFILL, B, S);
+    if (!ws || ws_bytes < w->total || !aligned16(ws))
+        return fail(KVP_E_WORKSPACE, "prefill: workspace needs %zu bytes (16-byte aligned), got %zu",
+                    w->total, ws ? ws_bytes : (size_t)0);
+    return KVP_OK;
+}
+
+}  // namespace
+
+extern "C" int kvp_prefill(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* ws,
+                           size_t ws_bytes, void* stream) {
+    Workspace w;
+    int rc = check_prefill_args(ctx, x, y, B, S, ws, ws_bytes, &w);
+    if (rc) return rc;
+    if ((rc = check_layers(ctx, 0, ctx->d.L))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)ws;
+    if (ctx->bf16() && (rc = timed(ctx, KVP_K_ROPE_TABLE, st, [&] {
+                            return check_hip(kvp::rope_table((float2*)(base + w.rope), S, ctx->d.d_h,
+                                                             ctx->d.rope_base, st),
+                                             "RoPE table");
+                        })))
+        return rc;
+    void* bufs[2] = {y, base + w.x};   // the last layer writes y
+    const int L = ctx->d.L;
+    const void* cur = x;
+    for (int l = 0; l < L; ++l) {
+        void* out = bufs[(L - 1 - l) & 1];
+        if ((rc = run_prefill_layer(ctx, l, cur, out, base + w.o, base, w, B, S, st))) return rc;
+        cur = out;
+    }
+    return ok();
+}
+
+extern "C" int kvp_layer_forward(kvp_ctx* ctx, int l, const void* x, void* attn_out, void* y, int B,
+                                 int S, void* ws, size_t ws_bytes, void* stream) {
+    Workspace w;
+    int rc = check_prefill_args(ctx, x, y, B, S, ws, ws_bytes, &w);
+    if (rc) return rc;
+    if (l < 0 || l >= ctx->d.L) return fail(KVP_E_INVALID_ARG, "kvp_layer_forward: layer %d out of range", l);
+    if (attn_out && !aligned16(attn_out))
+        return fail(KVP_E_INVALID_ARG, "kvp_layer_forward: attn_out must be 16-byte aligned");
+    if ((rc = check_layers(ctx, l, l + 1))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)ws;
+    if (ctx->bf16() && (rc = timed(ctx, KVP_K_ROPE_TABLE, st, [&] {
+                            return check_hip(kvp::rope_table((float2*)(base + w.rope), S, ctx->d.d_h,
+                                                             ctx->d.rope_base, st),
+                                             "RoPE table");
+                        })))
+        return rc;
+    return run_prefill_layer(ctx, l, x, y, attn_out ? attn_out : base + w.o, base, w, B, S, st);
+}
+
+extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
+                               void* y, int B, void* ws, size_t ws_bytes, void* stream) {
+    if (!ctx || !x || !y || !len_dev) return fail(KVP_E_INVALID_ARG, "decode: NULL argument");
+    if (x == y) return fail(KVP_E_INVALID_ARG, "decode: x and y must not alias");
+    if (!aligned16(x) || !aligned16(y)) return fail(KVP_E_INVALID_ARG, "decode: x, y must be 16-byte aligned");
+    if (B < 1 || max_len < 0) return fail(KVP_E_INVALID_ARG, "decode: B >= 1 and max_len >= 0 required");
+    if (B > ctx->d.max_batch) return fail(KVP_E_CAPACITY, "decode: B=%d > max_batch=%d", B, ctx->d.max_batch);
+    if (max_len >= ctx->d.kv_capacity)
+        return fail(KVP_E_CAPACITY, "decode: position %d does not fit kv_capacity=%d", max_len,
+                    ctx->d.kv_capacity);
+    if (ctx->bf16() && B > kDecodeMaxRows)
+        return fail(KVP_E_SHAPE, "decode: bf16 decode handles at most %d sequences per call", kDecodeMaxRows);
+    const Workspace w = layout(*ctx, KVP_PHASE_DECODE, B, 1);
+    if (!ws || ws_bytes < w.total || !aligned16(ws))
+        return fail(KVP_E_WORKSPACE, "decode: workspace needs %zu bytes (16-byte aligned), got %zu",
+                    w.total, ws ? ws_bytes : (size_t)0);
+    int rc;
+    if ((rc = check_layers(ctx, 0, ctx->d.L))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)ws;
+    void* bufs[2] = {y, base + w.x};
+    const int L = ctx->d.L;
+    const void* cur = x;
+    for (int l = 0; l < L; ++l) {
+        void* out = bufs[(L - 1 - l) & 1];
+        if ((rc = run_decode_layer(ctx, l, cur, out, len_dev, max_len, base, w, B, st))) return rc;
+        cur = out;
+    }
+    return ok();
+}

@@ -1,0 +1,300 @@
+// Smaller kernels of the path:
+//   rope_table    -- cos/sin of pos * theta_i in double, stored as fp32 pairs.
+//   rope_scatter  -- RoPE on fp32 projections, then Q to its buffer and K, V
+//                    (transposed) into the producer's slot; used by decode
+//                    (position len_b of each sequence) and by fp32 models.
+//   gemm_skinny   -- decode projections, M = batch <= 64 rows, bf16 MFMA;
+//                    HBM-bound on the weights.
+//   gemm_f32, attn_f32 -- the full-precision path for fp32 models (vector
+//                    ALU, no reduced-precision matrix modes).
+#include <math.h>
+
+#include "common.h"
+#include "kernels.h"
+
+namespace kvp {
+namespace {
+
+__device__ __forceinline__ const void* w_row_any(const WRows& w, int n, int K, int esize) {
+    const char* base;
+    if (n < w.rows[0]) {
+        base = (const char*)w.p[0];
+    } else if (n < w.rows[0] + w.rows[1]) {
+        n -= w.rows[0];
+        base = (const char*)w.p[1];
+    } else {
+        n -= w.rows[0] + w.rows[1];
+        base = (const char*)w.p[2];
+    }
+    return base + (size_t)n * K * esize;
+}
+
+// ---------------------------------------------------------------------------
+// RoPE
+// ---------------------------------------------------------------------------
+
+__global__ void rope_table_kernel(float2* t, int S, int half, int d, double base) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= S * half) return;
+    const int pos = idx / half, i = idx - pos * half;
+    const double theta = pow(base, -2.0 * i / d);
+    double s, c;
+    sincos((double)pos * theta, &s, &c);
+    t[idx] = make_float2((float)c, (float)s);
+}
+
+template <typename T>
+__device__ __forceinline__ void put(T* p, size_t i, float v);
+template <>
+__device__ __forceinline__ void put<float>(float* p, size_t i, float v) { p[i] = v; }
+template <>
+__device__ __forceinline__ void put<uint16_t>(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
+
+template <typename T>
+__global__ void rope_scatter_kernel(const float* __restrict__ proj, int S,
+                                    const int32_t* __restrict__ lens, int a, int g, int d, int cap,
+                                    double base, int producer, T* q, T* kc, T* vc) {
+    const int r = blockIdx.x;
+    int b, pos;
+    if (lens) {
+        b = r;
+        pos = max(0, min(lens[r], cap - 1));   // never outside the slot
+    } else {
+        b = r / S;
+        pos = r - b * S;
+    }
+    const int half = d / 2, nq = a * d, nkv = g * d;
+    const float* pr = proj + (size_t)r * (nq + (producer ? 2 * nkv : 0));
+    const int heads = a + (producer ? g : 0);
+    for (int j = threadIdx.x; j < heads * half; j += blockDim.x) {
+        const int h = j / half, i = j - h * half;
+        const double theta = pow(base, -2.0 * i / d);
+        double sd, cd;
+        sincos((double)pos * theta, &sd, &cd);
+        const float c = (float)cd, s = (float)sd;
+        const float x1 = pr[h * d + i], x2 = pr[h * d + i + half];
+        const float o1 = x1 * c - x2 * s, o2 = x2 * c + x1 * s;
+        if (h < a) {
+            put(q, (size_t)r * nq + h * d + i, o1);
+            put(q, (size_t)r * nq + h * d + i + half, o2);
+        } else {
+            const size_t kb = (((size_t)b * g + (h - a)) * cap + pos) * d;
+            put(kc, kb + i, o1);
+            put(kc, kb + i + half, o2);
+        }
+    }
+    if (producer) {
+        for (int j = threadIdx.x; j < nkv; j += blockDim.x) {
+            const int h = j / d, c = j - h * d;
+            put(vc, (((size_t)b * g + h) * d + c) * cap + pos, pr[nq + nkv + j]);
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Skinny bf16 GEMM for decode: a workgroup owns 16 output columns; its four
+// waves split K and meet in LDS at the end.
+// ---------------------------------------------------------------------------
+
+constexpr int SK_THREADS = 256;
+
+__global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(
+    const uint16_t* __restrict__ X, WRows W, int M, int N, int K, float* __restrict__ out,
+    const uint16_t* __restrict__ xres, uint16_t* __restrict__ y) {
+    __shared__ f32x4 red[4][4][64];   // [wave][m block][lane]
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int col = lane & 15, grp = lane >> 4;
+    const int n = blockIdx.x * 16 + col;
+    const uint16_t* wr = (const uint16_t*)w_row_any(W, min(n, N - 1), K, 2);
+    const int nmb = (M + 15) / 16;
+
+    const uint16_t* xr[4];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) xr[mb] = X + (size_t)min(16 * mb + col, M - 1) * K;
+
+    f32x4 acc[4];
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x4{};
+
+    // Wave w takes the 128-wide K chunks w, w + 4, w + 8, ... (K % 128 == 0).
+    for (int k = wave * 128; k < K; k += 512) {
+        u32x4 wf[4];
+#pragma unroll
+        for (int j = 0; j < 4; ++j) wf[j] = *(const u32x4*)(wr + k + 32 * j + 8 * grp);
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb) {
+            if (mb < nmb) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const u32x4 xf = *(const u32x4*)(xr[mb] + k + 32 * j + 8 * grp);
+                    acc[mb] = mfma16x16x32(as_bf16x8(xf), as_bf16x8(wf[j]), acc[mb]);
+                }
+            }
+        }
+    }
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) red[wave][mb][lane] = acc[mb];
+    __syncthreads();
+    if (wave != 0) return;
+#pragma unroll
+    for (int mb = 0; mb < 4; ++mb) {
+        if (mb >= nmb) break;
+        const f32x4 v = red[0][mb][lane] + red[1][mb][lane] + red[2][mb][lane] + red[3][mb][lane];
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int m = 16 * mb + 4 * grp + i;
+            if (m < M && n < N) {
+                const size_t off = (size_t)m * N + n;
+                if (out)
+                    out[off] = v[i];
+                else
+                    y[off] = f2bf(bf2f(xres[off]) + v[i]);
+            }
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 path
+// ---------------------------------------------------------------------------
+
+__global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, WRows W, int M,
+                                                       int N, int K, float* __restrict__ out,
+                                                       const float* __restrict__ xres) {
+    __shared__ float As[16][68], Ws[16][68];
+    const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
+    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
+    float acc[4][4] = {};
+    for (int k0 = 0; k0 < K; k0 += 16) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            const int id = tid + 256 * i, row = id >> 4, kk = id & 15;
+            const int m = m0 + row, n = n0 + row, k = k0 + kk;
+            As[kk][row] = (m < M && k < K) ? A[(size_t)m * K + k] : 0.f;
+            Ws[kk][row] = (n < N && k < K) ? ((const float*)w_row_any(W, n, K, 4))[k] : 0.f;
+        }
+        __syncthreads();
+#pragma unroll
+        for (int kk = 0; kk < 16; ++kk) {
+            float av[4], bv[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                av[i] = As[kk][ty * 4 + i];
+                bv[i] = Ws[kk][tx * 4 + i];
+            }
+#pragma unroll
+            for (int i = 0; i < 4; ++i)
+#pragma unroll
+                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+        }
+        __syncthreads();
+    }
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+            if (m < M && n < N) {
+                const size_t off = (size_t)m * N + n;
+                out[off] = xres ? xres[off] + acc[i][j] : acc[i][j];
+            }
+        }
+}
+
+template <int D>
+__global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ q,
+                                                      const float* __restrict__ kc,
+                                                      const float* __restrict__ vc,
+                                                      const int32_t* __restrict__ lens,
+                                                      float* __restrict__ o, int rows, int S, int a,
+                                                      int g, int cap) {
+    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
+    if (idx >= rows * a) return;
+    const int r = idx / a, h = idx - r * a, kvh = h / (a / g);
+    int b, pos;
+    if (lens) {
+        b = r;
+        pos = max(0, min(lens[r], cap - 1));
+    } else {
+        b = r / S;
+        pos = r - b * S;
+    }
+    const float scale = 1.0f / sqrtf((float)D);
+    float qv[D], acc[D];
+#pragma unroll
+    for (int i = 0; i < D; ++i) {
+        qv[i] = q[((size_t)r * a + h) * D + i];
+        acc[i] = 0.f;
+    }
+    const float* kb = kc + ((size_t)b * g + kvh) * cap * D;
+    const float* vb = vc + ((size_t)b * g + kvh) * D * cap;
+    float m = -INFINITY, l = 0.f;
+    for (int t = 0; t <= pos; ++t) {
+        float s = 0.f;
+#pragma unroll
+        for (int i = 0; i < D; ++i) s = fmaf(qv[i], kb[(size_t)t * D + i], s);
+        s *= scale;
+        const float m_new = fmaxf(m, s);
+        const float alpha = expf(m - m_new), p = expf(s - m_new);
+        l = l * alpha + p;
+#pragma unroll
+        for (int i = 0; i < D; ++i) acc[i] = acc[i] * alpha + p * vb[(size_t)i * cap + t];
+        m = m_new;
+    }
+    const float inv = 1.0f / l;
+#pragma unroll
+    for (int i = 0; i < D; ++i) o[((size_t)r * a + h) * D + i] = acc[i] * inv;
+}
+
+}  // namespace
+
+hipError_t rope_table(float2* table, int S, int d, double base, hipStream_t st) {
+    const int n = S * (d / 2);
+    hipLaunchKernelGGL(rope_table_kernel, dim3((n + 255) / 256), dim3(256), 0, st, table, S, d / 2, d,
+                       base);
+    return hipGetLastError();
+}
+
+hipError_t rope_scatter(const float* proj, int rows, int S, const int32_t* lens, int a, int g,
+                        int d, int cap, double base, bool producer, bool bf16, void* q, void* kc,
+                        void* vc, hipStream_t st) {
+    if (rows <= 0) return hipSuccess;
+    if (bf16)
+        hipLaunchKernelGGL(rope_scatter_kernel<uint16_t>, dim3(rows), dim3(256), 0, st, proj, S, lens,
+                           a, g, d, cap, base, producer ? 1 : 0, (uint16_t*)q, (uint16_t*)kc,
+                           (uint16_t*)vc);
+    else
+        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(rows), dim3(256), 0, st, proj, S, lens, a,
+                           g, d, cap, base, producer ? 1 : 0, (float*)q, (float*)kc, (float*)vc);
+    return hipGetLastError();
+}
+
+hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
+                            float* out_f32, const uint16_t* x_res, uint16_t* y, hipStream_t st) {
+    hipLaunchKernelGGL(gemm_skinny_kernel, dim3((N + 15) / 16), dim3(SK_THREADS), 0, st, x, w, M, N, K,
+                       out_f32, x_res, y);
+    return hipGetLastError();
+}
+
+hipError_t gemm_f32(const float* a, const WRows& w, int M, int N, int K, float* out,
+                    const float* x_res, hipStream_t st) {
+    dim3 grid((N + 63) / 64, (M + 63) / 64);
+    hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, st, a, w, M, N, K, out, x_res);
+    return hipGetLastError();
+}
+
+hipError_t attn_f32(const float* q, const float* kc, const float* vc, const int32_t* lens, float* o,
+                    int rows, int S, int a, int g, int d, int cap, hipStream_t st) {
+    const int n = rows * a;
+    dim3 grid((n + 63) / 64), block(64);
+    switch (d) {
+        case 16: hipLaunchKernelGGL(attn_f32_kernel<16>, grid, block, 0, st, q, kc, vc, lens, o, rows, S, a, g, cap); break;
+        case 32: hipLaunchKernelGGL(attn_f32_kernel<32>, grid, block, 0, st, q, kc, vc, lens, o, rows, S, a, g, cap); break;
+        case 64: hipLaunchKernelGGL(attn_f32_kernel<64>, grid, block, 0, st, q, kc, vc, lens, o, rows, S, a, g, cap); break;
+        case 128: hipLaunchKernelGGL(attn_f32_kernel<128>, grid, block, 0, st, q, kc, vc, lens, o, rows, S, a, g, cap); break;
+        default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+}  // namespace kvp

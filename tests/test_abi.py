@@ -1,0 +1,202 @@
+"""The C ABI library on the CPU: it loads, exports every symbol that
+include/kvpipe.h declares, its planner reproduces the oracle bit for bit, and
+its host-side argument checks return the documented status codes.  Nothing
+here launches a GPU kernel."""
+import os
+import random
+import re
+
+import pytest
+
+from oracle import planner as opl
+from paper_2608_15943_amd import binding as kb
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_functions():
+    names = []
+    for fn in os.listdir(os.path.join(ROOT, "include")):
+        if fn.endswith(".h"):
+            src = open(os.path.join(ROOT, "include", fn)).read()
+            src = re.sub(r"/\*.*?\*/", "", src, flags=re.S)
+            names += re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(kvp_\w+)\s*\(", src, flags=re.M)
+    return sorted(set(names))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert len(names) >= 16
+    lib = kb.lib()
+    for n in names:
+        assert hasattr(lib, n), n
+    assert sorted(kb.EXPORTS) == names
+
+
+def test_status_strings():
+    assert kb.status_name(kb.KVP_E_BAD_MAP) == "KVP_E_BAD_MAP"
+    assert kb.status_name(0) == "KVP_OK"
+
+
+# ---------------------------------------------------------------------------
+# Planner: C++ vs the oracle, same IEEE double operations in the same order.
+# ---------------------------------------------------------------------------
+
+def _compare_plans(stage, ff, fs, lm, eps, m=0, adm=None, alpha=-1.0):
+    P = max(stage) + 1
+    ref = opl.plan_fir(stage, P, ff, fs, lm, eps, m=m, admissible=adm, alpha=alpha)
+    got = kb.kvp_plan_fir(stage, ff, fs, lm, eps, m=m, admissible=adm, alpha=alpha, P=P)
+    assert got["z"] == ref.z
+    assert got["stage_flops"] == ref.stage_flops          # exact, not approximate
+    assert got["fir"] == ref.fir
+    assert got["n_converted"] == ref.n_converted
+    assert got["stop_reason"] == ref.stop_reason
+    return got
+
+
+def test_planner_llama2_pp8_matches_oracle_and_paper():
+    f0, f1 = kb.kvp_layer_flops(1, 8192, 4096, 32, 32, ffn=11008, causal=True)
+    assert (f0, f1) == tuple(float(v) for v in opl.layer_flops_prefill(1, 8192, 4096, 32, 32, ffn=11008))
+    stage = [l // 4 for l in range(32)]
+    lm = 2.0 * 8192 * 4096 * 32000
+    got = _compare_plans(stage, [f0] * 32, [f1] * 32, lm, eps=0.02, m=4)
+    assert [l + 1 for l in range(32) if got["z"][l]] == [29, 30, 31, 32]
+    assert abs(got["fir"] - 1.00040391) < 2e-5
+
+
+def test_planner_toys_and_guardrail():
+    toy = [l // 3 for l in range(12)]
+    _compare_plans(toy, [10] * 12, [7] * 12, 6, 0.01)
+    _compare_plans(toy, [10] * 12, [7] * 12, 9, 0.01)
+    got = _compare_plans(toy, [10] * 12, [4] * 12, 4, 0.01, m=3)
+    assert [l for l in range(12) if got["z"][l]] == [5, 8, 11]
+    _compare_plans(toy, [10] * 12, [9] * 12, 30, 0.01, adm=[False] * 11 + [True])
+    _compare_plans([l // 4 for l in range(32)], [100.0] * 32, [90.0] * 32, 500.0, 0.001, alpha=0.5)
+
+
+def test_planner_random_property():
+    rng = random.Random(1234)
+    for _ in range(300):
+        L = rng.randint(1, 40)
+        P = rng.randint(1, L)
+        cuts = sorted(rng.sample(range(1, L), P - 1)) if P > 1 else []
+        stage, s = [], 0
+        for l in range(L):
+            if s < len(cuts) and l >= cuts[s]:
+                s += 1
+            stage.append(s)
+        ff = [rng.uniform(1e9, 1e12) for _ in range(L)]
+        fs = [f * rng.uniform(0.5, 0.99) for f in ff]
+        lm = rng.uniform(0, 5e12)
+        eps = rng.choice([1e-6, 1e-3, 0.01, 0.05, 0.2])
+        m = rng.randint(0, L)
+        adm = [rng.random() < 0.8 for _ in range(L)] if rng.random() < 0.5 else None
+        alpha = rng.choice([-1.0, 0.0, 0.25, 0.5, 0.9])
+        _compare_plans(stage, ff, fs, lm, eps, m=m, adm=adm, alpha=alpha)
+
+
+def test_fir_and_layer_flops_closed_forms():
+    assert kb.kvp_fir([30, 30, 30, 36]) == 36 / 31.5
+    f0, f1 = kb.kvp_layer_flops(64, 32768, 4096, 32, 8, phase=kb.KVP_PHASE_DECODE)
+    assert (f0, f1) == tuple(float(v) for v in opl.layer_flops_decode(64, 32768, 4096, 32, 8))
+    f0, f1 = kb.kvp_layer_flops(4, 4096, 2048, 16, 8, causal=False)
+    assert f0 == 4 * 4 * 4096 * 2048 ** 2 + 4 * 4 * 4096 * 2048 ** 2 / 2 + 4 * 4 * 4096 ** 2 * 2048
+
+
+def test_planner_rejections():
+    with pytest.raises(kb.KvpError) as e:
+        kb.kvp_plan_fir([0, 1, 1], [1, 1, 1], [0.5] * 3, 0, eps=0.0)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    with pytest.raises(kb.KvpError):        # decreasing stage index
+        kb.kvp_plan_fir([0, 1, 0], [1] * 3, [0.5] * 3, 0, eps=0.1, P=2)
+    with pytest.raises(kb.KvpError):        # skipped stage
+        kb.kvp_plan_fir([0, 2, 2], [1] * 3, [0.5] * 3, 0, eps=0.1, P=3)
+    with pytest.raises(kb.KvpError):        # F(0) - F(1) <= 0 on an admissible layer
+        kb.kvp_plan_fir([0, 1], [1, 1], [1, 1], 0, eps=0.1)
+    with pytest.raises(kb.KvpError):        # P > L
+        kb.kvp_plan_fir([0], [1], [0.5], 0, eps=0.1, P=2)
+
+
+def test_maps():
+    assert kb.kvp_map_from_mask([0, 0, 0, 0, 0, 1, 0, 1]) == [0, 1, 2, 3, 4, 4, 6, 6]
+    assert kb.kvp_map_from_mask([0, 1, 1, 1]) == opl.map_from_mask([0, 1, 1, 1])
+    with pytest.raises(kb.KvpError) as e:
+        kb.kvp_map_from_mask([1, 0])
+    assert e.value.code == kb.KVP_E_BAD_MAP
+    assert kb.kvp_canonicalize_map([0, 0, 1, 2, 4]) == [0, 0, 0, 0, 4]
+    for bad in ([1], [0, 2, 2], [0, -1]):
+        with pytest.raises(kb.KvpError) as e:
+            kb.kvp_canonicalize_map(bad)
+        assert e.value.code == kb.KVP_E_BAD_MAP
+
+
+# ---------------------------------------------------------------------------
+# Context and host-side argument checks (no kernel launches).
+# ---------------------------------------------------------------------------
+
+def _model(**kw):
+    args = dict(L=4, h=256, a=2, g=1, d_h=128, dtype=kb.KVP_DTYPE_BF16, tau=[0, 0, 2, 2],
+                max_batch=2, max_seq=64, kv_capacity=128)
+    args.update(kw)
+    return kb.Model(**args)
+
+
+def test_create_validates_shape_and_map():
+    m = _model(tau=[0, 1, 1, 2])
+    assert m.kvp_get_map() == [0, 1, 1, 1]          # chains resolved
+    for kw, code in [(dict(tau=[1, 0, 2, 2]), kb.KVP_E_BAD_MAP),
+                     (dict(tau=[0, 3, 2, 2]), kb.KVP_E_BAD_MAP),
+                     (dict(d_h=64, a=4), kb.KVP_E_SHAPE),
+                     (dict(kv_capacity=100), kb.KVP_E_SHAPE),
+                     (dict(g=3), kb.KVP_E_INVALID_ARG),
+                     (dict(h=300), kb.KVP_E_INVALID_ARG),
+                     (dict(max_seq=256), kb.KVP_E_INVALID_ARG),
+                     (dict(dtype=7), kb.KVP_E_INVALID_ARG),
+                     (dict(dtype=kb.KVP_DTYPE_FP32, d_h=48, a=4, h=192), kb.KVP_E_SHAPE)]:
+        with pytest.raises(kb.KvpError) as e:
+            _model(**kw)
+        assert e.value.code == code, kw
+
+
+def test_set_layer_and_slot_rules():
+    m = _model()
+    fake = 1 << 20                                    # never dereferenced on the host
+    m.kvp_set_layer(0, fake, fake, fake, fake)
+    with pytest.raises(kb.KvpError) as e:            # consumer with its own K/V weights
+        m.kvp_set_layer(1, fake, fake, fake, fake)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    with pytest.raises(kb.KvpError):                 # producer without Wk
+        m.kvp_set_layer(2, fake, 0, fake, fake)
+    with pytest.raises(kb.KvpError):                 # consumers own no slot
+        m.kvp_set_kv_slot(1, fake, fake)
+    with pytest.raises(kb.KvpError):                 # misaligned
+        m.kvp_set_layer(1, fake + 2, 0, 0, fake)
+
+
+def test_workspace_and_call_checks():
+    m = _model()
+    n = m.kvp_workspace_size(kb.KVP_PHASE_PREFILL, 2, 64)
+    assert n > 2 * 64 * 256 * 2 * 3
+    with pytest.raises(kb.KvpError) as e:
+        m.kvp_workspace_size(kb.KVP_PHASE_PREFILL, 3, 64)
+    assert e.value.code == kb.KVP_E_CAPACITY
+    fake = 1 << 20
+    with pytest.raises(kb.KvpError) as e:            # weights never set
+        m.kvp_prefill(fake, fake * 2, 2, 64, fake * 4, n)
+    assert e.value.code == kb.KVP_E_STATE
+    with pytest.raises(kb.KvpError) as e:            # workspace too small
+        m.kvp_prefill(fake, fake * 2, 2, 64, fake * 4, n - 1)
+    assert e.value.code == kb.KVP_E_WORKSPACE
+    with pytest.raises(kb.KvpError) as e:            # S > max_seq
+        m.kvp_prefill(fake, fake * 2, 2, 65, fake * 4, n)
+    assert e.value.code == kb.KVP_E_CAPACITY
+    with pytest.raises(kb.KvpError) as e:            # aliasing x and y
+        m.kvp_prefill(fake, fake, 2, 64, fake * 4, n)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    nd = m.kvp_workspace_size(kb.KVP_PHASE_DECODE, 2)
+    with pytest.raises(kb.KvpError) as e:            # position does not fit the slot
+        m.kvp_decode_step(fake, fake * 8, 128, fake * 2, 2, fake * 4, nd)
+    assert e.value.code == kb.KVP_E_CAPACITY
+    with pytest.raises(kb.KvpError) as e:            # B > max_batch
+        m.kvp_decode_step(fake, fake * 8, 10, fake * 2, 3, fake * 4, nd)
+    assert e.value.code == kb.KVP_E_CAPACITY
