@@ -6,25 +6,28 @@
 //
 // Workgroup = 4 waves = 128 queries of one (sequence, head); wave w owns 32
 // queries.  Keys and values stream through LDS in tiles of 64 positions
-// (K: [64][128], V^T: [128][64]; 32 KB per tile, double buffered).
+// (K: [64][128], V^T: [128][64]; 32 KB per tile, double buffered), loaded
+// straight from HBM/L2 into LDS (global_load_lds_dwordx4): no staging
+// registers, and the XOR swizzle of the LDS rows is produced by choosing which
+// 16-byte chunk each lane fetches.
 //
 // Per tile and wave:
-//   S^T[64 x 32] = K_tile Q^T   v_mfma_f32_32x32x16_bf16, A = K from LDS,
+//   S^T[64 x 32] = K_tile Q^T   v_mfma_f32_32x32x16_bf16, A = K rows from LDS,
 //                               B = Q^T held in registers for the whole kernel.
-//   The lane that owns query q holds 32 of its 64 scores; the other 32 are in
-//   lane q ^ 32, so the row maximum needs one exchange and the row sum none
-//   (each lane keeps a partial sum, added at the end).
-//   P is rounded to bf16 and used as the B operand of
-//   O^T[128 x 32] += V^T_tile P^T  straight from the score registers: the
-//   positions a lane holds for a 16-wide k step are the ones it reads from the
-//   V^T tile (two 8-byte reads), so P never leaves registers.
-// Online softmax in the exp2 domain with a lazily moved maximum: the
-// accumulators are rescaled only when some row's maximum grows by more than
-// 8 (a factor 256), which keeps every exp2 argument <= 8.
+//   MFMA row rho of a 32-row block reads the K row whose index has bits 2 and
+//   3 of rho swapped; then the 8 scores a lane holds for each 16-position k
+//   step of the PV product are 8 consecutive positions, i.e. one 16-byte
+//   chunk of a V^T row, and P is used as the B operand of
+//   O^T[128 x 32] += V^T_tile P^T straight from the score registers.
+//   The lane that owns query q holds 32 of its 64 scores (the other 32 are in
+//   lane q ^ 32): the row max needs one exchange, the row sum none.
+// Online softmax in the exp2 domain with a lazily moved maximum: accumulators
+// are rescaled only when some row's maximum grows by more than 8 (a factor
+// 256), which keeps every exp2 argument <= 8.
 //
 // Query tiles are issued heaviest-first (most key tiles under the causal
-// mask) and grouped per XCD so that the r heads that share a KV head and
-// their key tiles meet in one L2.
+// mask) and grouped per XCD so that the r heads sharing a KV head and their
+// key tiles meet in one L2.
 #include <math.h>
 
 #include "common.h"
@@ -36,16 +39,23 @@ namespace {
 constexpr int BQ = 128, BKV = 64, D = 128, NT = 256;
 constexpr float kLazy = 8.0f;
 
-struct Tile {
-    u32x4 k[4];   // K: 64 rows x 16 chunks = 1024 chunks, 4 per thread
-    u32x4 v[4];   // V^T: 128 rows x 8 chunks = 1024 chunks, 4 per thread
-};
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
+// 64 lanes x 16 bytes from per-lane global addresses to 1 KB of LDS at lds_base
+// (wave-uniform): lane i lands at lds_base + 16 i.
+__device__ __forceinline__ void load_lds_1k(const void* gsrc, void* lds_base) {
+    __builtin_amdgcn_global_load_lds((gvoid_t*)gsrc, (lvoid_t*)lds_base, 16, 0, 0);
+}
+
+__device__ __forceinline__ int swap_b23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
 __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int B, int S, int a, int g, int cap, float scale_log2) {
-    __shared__ u32x4 lk[2][BKV * 16];   // [stage][row * 16 + (chunk ^ (row & 15))]
-    __shared__ u32x2 lv[2][D * 16];     // [stage][d * 16 + (unit ^ (d & 15))], unit = 4 positions
+    // K: [stage][row * 16 + (chunk ^ (row & 15))]; V^T: [stage][d * 8 + (chunk ^ (d & 7))].
+    __shared__ u32x4 lk[2][BKV * 16];
+    __shared__ u32x4 lv[2][D * 8];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, hi = lane >> 5;
@@ -78,41 +88,32 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     const int last_q = min(qt * BQ + BQ - 1, S - 1);
     const int ntiles = last_q / BKV + 1;
 
-    auto load_tile = [&](int t, Tile& tl) {
+    // Issue the 16 + 16 one-kilobyte loads of tile t (4 + 4 per wave).  They stay inside
+    // the slot: t0 + 64 <= cap (cap % 64 == 0 and t0 < S <= cap).
+    auto issue_tile = [&](int t, int stg) {
         const int t0 = t * BKV;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int id = tid + NT * i;
-            const int row = id >> 4, c = id & 15;     // K row = position, chunk of 8 dims
-            const int pos = t0 + row;
-            if (pos < S)
-                tl.k[i] = *(const u32x4*)(kbase + (size_t)pos * D + c * 8);
-            else
-                tl.k[i] = u32x4{0, 0, 0, 0};
-            const int d = id >> 3, vc = id & 7;       // V^T row = dim, chunk of 8 positions
-            const int p0 = t0 + vc * 8;
-            u32x4 v = *(const u32x4*)(vbase + (size_t)d * cap + p0);
-            if (p0 + 8 > S) {                         // zero positions >= S (never valid data)
-                const int keep = S - p0;              // 0..7 valid elements
-#pragma unroll
-                for (int e = 0; e < 4; ++e) {
-                    const int lo_ok = (2 * e) < keep, hi_ok = (2 * e + 1) < keep;
-                    v[e] &= (lo_ok ? 0x0000FFFFu : 0u) | (hi_ok ? 0xFFFF0000u : 0u);
-                }
-            }
-            tl.v[i] = v;
+        for (int j = 0; j < 4; ++j) {
+            const int r = 16 * wave + 4 * j + (lane >> 4);              // K row (position)
+            const int c = (lane & 15) ^ (r & 15);
+            load_lds_1k(kbase + (size_t)(t0 + r) * D + 8 * c, &lk[stg][(16 * wave + 4 * j) * 16]);
+            const int d = 32 * wave + 8 * j + (lane >> 3);               // V^T row (dim)
+            const int cv = (lane & 7) ^ (d & 7);
+            load_lds_1k(vbase + (size_t)d * cap + t0 + 8 * cv, &lv[stg][(32 * wave + 8 * j) * 8]);
         }
     };
-    auto store_tile = [&](int stg, const Tile& tl) {
+    // Positions >= S of the last tile may hold anything: zero their V (P is 0 there, but
+    // 0 * NaN is not).  K needs no fix-up: its scores are replaced by -inf.
+    auto fix_tail = [&](int t, int stg) {
+        const int t0 = t * BKV;
+        for (int i = tid; i < D * 8; i += NT) {
+            const int d = i >> 3, pc = i & 7, c = pc ^ (d & 7);
+            const int keep = S - (t0 + 8 * c);
+            u32x4 v = lv[stg][i];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int id = tid + NT * i;
-            const int row = id >> 4, c = id & 15;
-            lk[stg][row * 16 + (c ^ (row & 15))] = tl.k[i];
-            const int d = id >> 3, vc = id & 7;
-            const int u0 = 2 * vc, sw = d & 15;
-            lv[stg][d * 16 + (u0 ^ sw)] = u32x2{tl.v[i][0], tl.v[i][1]};
-            lv[stg][d * 16 + ((u0 + 1) ^ sw)] = u32x2{tl.v[i][2], tl.v[i][3]};
+            for (int e = 0; e < 4; ++e)
+                v[e] &= ((2 * e) < keep ? 0x0000FFFFu : 0u) | ((2 * e + 1) < keep ? 0xFFFF0000u : 0u);
+            lv[stg][i] = v;
         }
     };
 
@@ -121,36 +122,52 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     for (int i = 0; i < 4; ++i) o[i] = f32x16{};
     float m_run = -INFINITY, l_run = 0.f;
 
-    Tile nxt;
-    load_tile(0, nxt);
-    store_tile(0, nxt);
+    const int ksw = swap_b23(l32);          // K row read by this lane inside a 32-row block
+    issue_tile(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
+    if (BKV > S) {
+        fix_tail(0, 0);
+        __syncthreads();
+    }
 
     for (int t = 0; t < ntiles; ++t) {
         const int stg = t & 1;
-        if (t + 1 < ntiles) load_tile(t + 1, nxt);
+        if (t + 1 < ntiles) issue_tile(t + 1, stg ^ 1);
 
         const int t0 = t * BKV;
         if (t0 <= q0w + 31 && q0w < S) {          // some key of the tile is visible to this wave
-            // ---- S^T = K Q^T -------------------------------------------------------
+            // ---- S^T = K Q^T; K fragments are read two k steps ahead --------------------
             f32x16 s[2] = {f32x16{}, f32x16{}};
+            bf16x8 kf[3][2];
+            auto kfrag = [&](int mb, int ks) {
+                const int row = 32 * mb + ksw;
+                return as_bf16x8(lk[stg][row * 16 + ((2 * ks + hi) ^ (row & 15))]);
+            };
+#pragma unroll
+            for (int ks = 0; ks < 2; ++ks) {
+                kf[ks][0] = kfrag(0, ks);
+                kf[ks][1] = kfrag(1, ks);
+            }
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
-                const int c = 2 * ks + hi;
-#pragma unroll
-                for (int mb = 0; mb < 2; ++mb) {
-                    const int row = 32 * mb + l32;
-                    s[mb] = mfma32x32x16(as_bf16x8(lk[stg][row * 16 + (c ^ (row & 15))]), qf[ks], s[mb]);
+                if (ks + 2 < 8) {
+                    kf[(ks + 2) % 3][0] = kfrag(0, ks + 2);
+                    kf[(ks + 2) % 3][1] = kfrag(1, ks + 2);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // 2 LDS reads, then
                 }
+                s[0] = mfma32x32x16(kf[ks % 3][0], qf[ks], s[0]);
+                s[1] = mfma32x32x16(kf[ks % 3][1], qf[ks], s[1]);
+                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);       // 2 MFMAs
             }
-            // ---- mask: position > query (causal) or >= S ----------------------------
+            // Register i of block mb holds position t0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
             const bool diag = (t0 + BKV - 1 > q0w) || (t0 + BKV > S);
             if (diag) {
 #pragma unroll
                 for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
                     for (int i = 0; i < 16; ++i) {
-                        const int pos = t0 + 32 * mb + 8 * (i >> 2) + 4 * hi + (i & 3);
+                        const int pos = t0 + 32 * mb + 16 * (i >> 3) + 8 * hi + (i & 7);
                         if (pos > q_lane || pos >= S) s[mb][i] = -INFINITY;
                     }
             }
@@ -162,56 +179,66 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
             mx = fmaxf(mx, __shfl_xor(mx, 32));
             const float mt = mx * scale_log2;                  // tile max, log2 domain
-            const bool grow = mt > m_run + kLazy;
-            if (__any(grow)) {
+            if (__any(mt > m_run + kLazy)) {
                 const float m_new = fmaxf(m_run, mt);
                 const float alpha = exp2f(m_run - m_new);      // 0 on the first visible tile
                 m_run = m_new;
                 l_run *= alpha;
 #pragma unroll
-                for (int db = 0; db < 4; ++db)
-#pragma unroll
-                    for (int i = 0; i < 16; ++i) o[db][i] *= alpha;
+                for (int db = 0; db < 4; ++db) o[db] *= alpha;
             }
             bf16x8 pb[2][2];
 #pragma unroll
             for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-                for (int jp = 0; jp < 2; ++jp) {
-                    float p[8];
+                for (int p = 0; p < 2; ++p) {
+                    float e[8];
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        p[e] = exp2f(fmaf(s[mb][8 * jp + e], scale_log2, -m_run));
-                        l_run += p[e];
+                    for (int k = 0; k < 8; ++k) {
+                        e[k] = exp2f(fmaf(s[mb][8 * p + k], scale_log2, -m_run));
+                        l_run += e[k];
                     }
                     u32x4 w;
-                    w[0] = pack2bf(p[0], p[1]);
-                    w[1] = pack2bf(p[2], p[3]);
-                    w[2] = pack2bf(p[4], p[5]);
-                    w[3] = pack2bf(p[6], p[7]);
-                    pb[mb][jp] = as_bf16x8(w);
+                    w[0] = pack2bf(e[0], e[1]);
+                    w[1] = pack2bf(e[2], e[3]);
+                    w[2] = pack2bf(e[4], e[5]);
+                    w[3] = pack2bf(e[6], e[7]);
+                    pb[mb][p] = as_bf16x8(w);
                 }
-            // ---- O^T += V^T P^T -------------------------------------------------------
+            // ---- O^T += V^T P^T: 16 MFMAs, each V^T chunk read three MFMAs ahead -----------
+            auto vfrag = [&](int i) {
+                const int db = i >> 2, c = i & 3;                 // chunk c = 2 mb + p
+                const int d = 32 * db + l32;
+                return as_bf16x8(lv[stg][d * 8 + ((2 * c + hi) ^ (d & 7))]);
+            };
+            bf16x8 vf[4];
 #pragma unroll
-            for (int db = 0; db < 4; ++db) {
-                const int d = 32 * db + l32, sw = d & 15;
+            for (int i = 0; i < 3; ++i) vf[i] = vfrag(i);
 #pragma unroll
-                for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-                    for (int jp = 0; jp < 2; ++jp) {
-                        const int u1 = 8 * mb + 4 * jp + hi;     // positions 32mb + 16jp + 4hi + 0..3
-                        const u32x2 lo = lv[stg][d * 16 + (u1 ^ sw)];
-                        const u32x2 up = lv[stg][d * 16 + ((u1 + 2) ^ sw)];
-                        const u32x4 w = {lo[0], lo[1], up[0], up[1]};
-                        o[db] = mfma32x32x16(as_bf16x8(w), pb[mb][jp], o[db]);
-                    }
+            for (int i = 0; i < 16; ++i) {
+                if (i + 3 < 16) {
+                    vf[(i + 3) & 3] = vfrag(i + 3);
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+                }
+                const int db = i >> 2, mb = (i >> 1) & 1, p = i & 1;
+                o[db] = mfma32x32x16(vf[i & 3], pb[mb][p], o[db]);
+                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             }
         }
-        if (t + 1 < ntiles) store_tile(stg ^ 1, nxt);
-        __syncthreads();
+        // One barrier: tile t + 1 has landed in LDS (every wave waited for its own loads)
+        // and every wave is done reading tile t, whose buffer is refilled next.
+        if (t + 1 < ntiles) {
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+            __syncthreads();
+            if ((t + 2) * BKV > S) {
+                fix_tail(t + 1, stg ^ 1);
+                __syncthreads();
+            }
+        }
     }
 
     // ---- normalise and store O[b, q, head, :] -------------------------------------
+    // Lanes q and q ^ 32 hold the same query, so both take this branch or neither.
     if (q_lane < S) {
         const float l_tot = l_run + __shfl_xor(l_run, 32);
         const float inv = 1.0f / l_tot;
@@ -226,8 +253,6 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 w[1] = pack2bf(o[db][4 * r4 + 2] * inv, o[db][4 * r4 + 3] * inv);
                 *(u32x2*)(orow + d0) = w;
             }
-    } else {
-        (void)__shfl_xor(l_run, 32);
     }
 }
 

@@ -63,7 +63,10 @@ struct QkvEpi {
                         } else {
                             for (int r = 0; r < 4 && mrow0 + r < M; ++r) {
                                 int b = b0, s = s0 + r;
-                                if (s >= o.S) { s -= o.S; ++b; }
+                                while (s >= o.S) {  // 4 rows can span several sequences when S < 4
+                                    s -= o.S;
+                                    ++b;
+                                }
                                 o.vc[(((size_t)b * o.g + head) * 128 + c) * o.cap + s] =
                                     f2bf(acc[mb][nb][4 * r4 + r]);
                             }
@@ -86,7 +89,10 @@ struct QkvEpi {
                     const int m = mrow0 + r;
                     if (m >= M) break;
                     int b = b0, s = s0 + r;
-                    if (s >= o.S) { s -= o.S; ++b; }
+                    while (s >= o.S) {  // 4 rows can span several sequences when S < 4
+                        s -= o.S;
+                        ++b;
+                    }
                     uint16_t* dst = is_q ? o.q + (size_t)m * o.n_q + head * 128
                                          : o.kc + (((size_t)b * o.g + head) * o.cap + s) * 128;
 #pragma unroll
@@ -175,35 +181,59 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
 
     const int nk = K / BK;
     const int l32 = lane & 31, hi = lane >> 5;
+    // LDS offsets (in 16-byte chunks) of this lane's fragment rows; row & 7 == l32 & 7.
+    int a_off[4], b_off[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+        a_off[i] = (wm * 128 + 32 * i + l32) * 8;
+        b_off[i] = (wn * 128 + 32 * i + l32) * 8;
+    }
+    const int sw = l32 & 7;
+    auto load_frags = [&](int stg, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
+        const int c = (2 * ks + hi) ^ sw;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            fa[i] = as_bf16x8(lds[stg][0][a_off[i] + c]);
+            fb[i] = as_bf16x8(lds[stg][1][b_off[i] + c]);
+        }
+    };
+
+    bf16x8 fa[4], fb[4], ga[4], gb[4];
+    load_frags(0, 0, fa, fb);
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt & 1;
-        if (kt + 1 < nk) {
+        const bool more = kt + 1 < nk;
+        if (more) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 ra[i] = a_src[i][(kt + 1) * 8];
                 rw[i] = w_src[i][(kt + 1) * 8];
             }
         }
+        // Four 16-wide k steps; the fragments of step ks + 1 are read from LDS while the
+        // 16 MFMAs of step ks run (one ds_read slotted after each of the first 8 MFMAs).
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
-            const int c = 2 * ks + hi;
-            bf16x8 af[4], bw[4];
-#pragma unroll
-            for (int mb = 0; mb < 4; ++mb) {
-                const int row = wm * 128 + 32 * mb + l32;
-                af[mb] = as_bf16x8(lds[cur][0][row * 8 + (c ^ (row & 7))]);
-            }
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb) {
-                const int row = wn * 128 + 32 * nb + l32;
-                bw[nb] = as_bf16x8(lds[cur][1][row * 8 + (c ^ (row & 7))]);
-            }
+            if (ks < 3) load_frags(cur, ks + 1, ga, gb);
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-                for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma32x32x16(af[mb], bw[nb], acc[mb][nb]);
+                for (int nb = 0; nb < 4; ++nb) acc[mb][nb] = mfma32x32x16(fa[mb], fb[nb], acc[mb][nb]);
+            if (ks < 3) {
+#pragma unroll
+                for (int i = 0; i < 8; ++i) {
+                    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // 1 MFMA
+                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // 1 LDS read
+                }
+                __builtin_amdgcn_sched_group_barrier(0x008, 8, 0);
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    fa[i] = ga[i];
+                    fb[i] = gb[i];
+                }
+            }
         }
-        if (kt + 1 < nk) {
+        if (more) {
 #pragma unroll
             for (int i = 0; i < 8; ++i) {
                 lds[cur ^ 1][0][soff[i]] = ra[i];
@@ -211,6 +241,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
             }
         }
         __syncthreads();
+        if (more) load_frags(cur ^ 1, 0, fa, fb);
     }
     epi(acc, m0 + wm * 128, n0 + wn * 128, lane, M, N);
 }

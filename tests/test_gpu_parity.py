@@ -76,6 +76,7 @@ def test_fp32_ragged_two_sequences():
     (512, 4, 1, [0, 0, 0], 1, 333),          # r=4, consumers only after layer 0
     (1024, 8, 1, [0, 0], 1, 130),            # r=8, S just past a query tile
     (256, 2, 1, [0, 1], 3, 1),               # S = 1
+    (256, 2, 1, [0, 1], 5, 3),               # S < 4: one 4-row group spans sequences
 ])
 def test_bf16_stack(h, a, g, tau, B, S):
     w = small_workload(f"bf16-h{h}-a{a}-g{g}", len(tau), h, a, g, tau)
