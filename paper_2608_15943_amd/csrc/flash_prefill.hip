@@ -53,7 +53,7 @@ __device__ __forceinline__ int swap_b23(int r) { return (r & ~12) | ((r & 4) << 
 __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, int B, int S, int a, int g, int cap, float scale_log2) {
-    // K: [stage][row * 16 + (chunk ^ (row & 15))]; V^T: [stage][d * 8 + (chunk ^ (d & 7))].
+    // K: [stage][row * 16 + (chunk ^ (row & 15))]; V^T: [stage][d * 8 + (chunk ^ ((d >> 1) & 7))].
     __shared__ u32x4 lk[2][BKV * 16];
     __shared__ u32x4 lv[2][D * 8];
 
@@ -98,7 +98,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             const int c = (lane & 15) ^ (r & 15);
             load_lds_1k(kbase + (size_t)(t0 + r) * D + 8 * c, &lk[stg][(16 * wave + 4 * j) * 16]);
             const int d = 32 * wave + 8 * j + (lane >> 3);               // V^T row (dim)
-            const int cv = (lane & 7) ^ (d & 7);
+            const int cv = (lane & 7) ^ ((d >> 1) & 7);
             load_lds_1k(vbase + (size_t)d * cap + t0 + 8 * cv, &lv[stg][(32 * wave + 8 * j) * 8]);
         }
     };
@@ -107,7 +107,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     auto fix_tail = [&](int t, int stg) {
         const int t0 = t * BKV;
         for (int i = tid; i < D * 8; i += NT) {
-            const int d = i >> 3, pc = i & 7, c = pc ^ (d & 7);
+            const int d = i >> 3, pc = i & 7, c = pc ^ ((d >> 1) & 7);
             const int keep = S - (t0 + 8 * c);
             u32x4 v = lv[stg][i];
 #pragma unroll
@@ -209,7 +209,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             auto vfrag = [&](int i) {
                 const int db = i >> 2, c = i & 3;                 // chunk c = 2 mb + p
                 const int d = 32 * db + l32;
-                return as_bf16x8(lv[stg][d * 8 + ((2 * c + hi) ^ (d & 7))]);
+                return as_bf16x8(lv[stg][d * 8 + ((2 * c + hi) ^ ((d >> 1) & 7))]);
             };
             bf16x8 vf[4];
 #pragma unroll

@@ -12,10 +12,10 @@
 //
 // Tiling: 256 x 256 x 64 per workgroup of 4 waves (2 x 2, 128 x 128 each, a
 // 4 x 4 grid of 32 x 32 MFMA blocks = 256 fp32 accumulators per lane).
-// Operand tiles go global -> registers -> LDS, double buffered (2 x 64 KB),
-// one barrier per K step; LDS rows are 128 B with the 16-byte chunk index
-// XOR-swizzled by (row & 7) so that the 32-row fragment reads spread over all
-// banks.  Tiles are ordered so that each XCD works on a contiguous group of
+// Operand tiles go straight from global memory into LDS (global_load_lds_dwordx4,
+// no staging registers), double buffered (2 x 64 KB), one barrier per K step;
+// LDS rows are 128 B with the 16-byte chunk index XOR-swizzled by
+// ((row >> 1) & 7), which spreads the 32-row fragment reads over all 64 banks.  Tiles are ordered so that each XCD works on a contiguous group of
 // M-panels (its own L2 keeps the A and W panels hot).
 #include "common.h"
 #include "kernels.h"
@@ -33,104 +33,219 @@ __device__ __forceinline__ const uint16_t* w_row(const WRows& w, int n, int K) {
     return (const uint16_t*)w.p[2] + (size_t)n * K;
 }
 
+// ---------------------------------------------------------------------------
+// Epilogues.  After the main loop each wave owns a 128 x 128 fp32 tile in
+// registers (lane: column n = 32 nb + l32, rows m = 32 mb + 8 (i/4) + 4 hi + i%4).
+// stage() writes it into the wave's 32 KB of the (now idle) LDS and flush()
+// copies it out with 16-byte coalesced global accesses, in Epi::kPasses passes.
+// ---------------------------------------------------------------------------
+
+// fp32 staging rows (128 x 64 fp32 = 256-byte rows, 16-byte chunk c): lanes write 128
+// contiguous bytes of rows m and m + 4, and read one chunk of 4 rows per 16 lanes; this
+// XOR keeps both patterns free of bank conflicts on the 64-bank LDS.
+__device__ __forceinline__ int f32_pos(int m, int c) {
+    return c ^ ((m & 1) | ((((m >> 1) ^ (m >> 2)) & 1) << 3));
+}
+__device__ __forceinline__ void st_f32(char* st, int m, int n, float v) {
+    *(float*)(st + m * 256 + f32_pos(m, n >> 2) * 16 + (n & 3) * 4) = v;
+}
+__device__ __forceinline__ u32x4 ld_f32(const char* st, int m, int c) {
+    return *(const u32x4*)(st + m * 256 + f32_pos(m, c) * 16);
+}
+
+// Q, K (rotated) and V (transposed) of the projection GEMM.  Q/K tiles go through LDS as
+// fp32 in two passes; pass h holds head columns 32 h .. 32 h + 31 and their rotate-half
+// partners 64 + 32 h .. 64 + 32 h + 31, so RoPE is applied in the flush with the cos/sin
+// of each (position, column) read as contiguous table rows.  V is staged once, in bf16,
+// transposed ([n][m], 8-byte unit u of row n at position u ^ (n & 31)).
 struct QkvEpi {
+    static constexpr int kPasses = 2;
     QkvOut o;
-    __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int mw, int nw, int lane, int M,
-                                               int N) const {
-        if (nw >= N) return;
+    // Region of the wave's 128 columns: 0 = Q, 1 = K, 2 = V, -1 = past N.
+    __device__ __forceinline__ int region(int nw, int N, int* head) const {
+        if (nw >= N) return -1;
+        if (nw < o.n_q) { *head = nw >> 7; return 0; }
+        if (nw < o.n_q + o.n_kv) { *head = (nw - o.n_q) >> 7; return 1; }
+        *head = (nw - o.n_q - o.n_kv) >> 7;
+        return 2;
+    }
+    __device__ __forceinline__ void stage(int pass, f32x16 (&acc)[4][4], int mw, int nw, int lane,
+                                          int M, int N, char* st) const {
+        int head;
+        const int reg = region(nw, N, &head);
+        if (reg < 0) return;
         const int l32 = lane & 31, hi = lane >> 5;
-        if (nw >= o.n_q + o.n_kv) {
-            // V (not rotated), stored transposed: four consecutive rows of a lane are
-            // four consecutive positions, one 8-byte store when they share a sequence.
-            const int head = (nw - o.n_q - o.n_kv) >> 7;
+        if (reg == 2) {
+            if (pass != 0) return;
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-                for (int r4 = 0; r4 < 4; ++r4) {
-                    const int mrow0 = mw + 32 * mb + 8 * r4 + 4 * hi;
-                    if (mrow0 >= M) continue;
-                    const int b0 = mrow0 / o.S, s0 = mrow0 - b0 * o.S;
-                    const bool packed = (mrow0 + 3 < M) && (s0 + 3 < o.S) && ((s0 & 3) == 0) &&
-                                        ((o.cap & 3) == 0);
+                for (int r4 = 0; r4 < 4; ++r4)
 #pragma unroll
                     for (int nb = 0; nb < 4; ++nb) {
-                        const int c = 32 * nb + l32;
-                        if (packed) {
-                            u32x2 v;
-                            v.x = pack2bf(acc[mb][nb][4 * r4 + 0], acc[mb][nb][4 * r4 + 1]);
-                            v.y = pack2bf(acc[mb][nb][4 * r4 + 2], acc[mb][nb][4 * r4 + 3]);
-                            *(u32x2*)(o.vc + (((size_t)b0 * o.g + head) * 128 + c) * o.cap + s0) = v;
-                        } else {
-                            for (int r = 0; r < 4 && mrow0 + r < M; ++r) {
-                                int b = b0, s = s0 + r;
-                                while (s >= o.S) {  // 4 rows can span several sequences when S < 4
-                                    s -= o.S;
-                                    ++b;
-                                }
-                                o.vc[(((size_t)b * o.g + head) * 128 + c) * o.cap + s] =
-                                    f2bf(acc[mb][nb][4 * r4 + r]);
-                            }
-                        }
+                        const int n = 32 * nb + l32, u = 8 * mb + 2 * r4 + hi;
+                        u32x2 v;
+                        v[0] = pack2bf(acc[mb][nb][4 * r4 + 0], acc[mb][nb][4 * r4 + 1]);
+                        v[1] = pack2bf(acc[mb][nb][4 * r4 + 2], acc[mb][nb][4 * r4 + 3]);
+                        *(u32x2*)(st + n * 256 + ((u ^ (n & 31)) * 8)) = v;
                     }
-                }
             return;
         }
-        // Q or K: rotate the pair (c, c + 64) of each head by the position's angle.
-        const bool is_q = nw < o.n_q;
-        const int head = is_q ? (nw >> 7) : ((nw - o.n_q) >> 7);
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-            for (int r4 = 0; r4 < 4; ++r4) {
-                const int mrow0 = mw + 32 * mb + 8 * r4 + 4 * hi;
-                const int b0 = mrow0 / o.S, s0 = mrow0 - b0 * o.S;
-#pragma unroll
-                for (int r = 0; r < 4; ++r) {
-                    const int m = mrow0 + r;
-                    if (m >= M) break;
-                    int b = b0, s = s0 + r;
-                    while (s >= o.S) {  // 4 rows can span several sequences when S < 4
-                        s -= o.S;
-                        ++b;
-                    }
-                    uint16_t* dst = is_q ? o.q + (size_t)m * o.n_q + head * 128
-                                         : o.kc + (((size_t)b * o.g + head) * o.cap + s) * 128;
-#pragma unroll
-                    for (int nb = 0; nb < 2; ++nb) {
-                        const int c = 32 * nb + l32;
-                        const float2 cs = o.rope[(size_t)s * 64 + c];
-                        const float x1 = acc[mb][nb][4 * r4 + r], x2 = acc[mb][nb + 2][4 * r4 + r];
-                        dst[c] = f2bf(x1 * cs.x - x2 * cs.y);
-                        dst[c + 64] = f2bf(x2 * cs.x + x1 * cs.y);
+            for (int i = 0; i < 16; ++i) {
+                const int m = 32 * mb + 8 * (i >> 2) + 4 * hi + (i & 3);
+                st_f32(st, m, l32, pass == 0 ? acc[mb][0][i] : acc[mb][1][i]);
+                st_f32(st, m, 32 + l32, pass == 0 ? acc[mb][2][i] : acc[mb][3][i]);
+            }
+    }
+    __device__ __forceinline__ void flush(int pass, int mw, int nw, int lane, int M, int N,
+                                          const char* st) const {
+        int head;
+        const int reg = region(nw, N, &head);
+        if (reg < 0) return;
+        if (reg == 2) {
+            if (pass != 0) return;
+            // V^T rows: 16 lanes x 16 bytes = one 128-position row n.
+            const bool fast = (o.S % 8) == 0;
+#pragma unroll 4
+            for (int it = 0; it < 32; ++it) {
+                const int n = 4 * it + (lane >> 4), k = lane & 15;   // chunk k = positions 8k..8k+7
+                const int m = mw + 8 * k;
+                if (m >= M) continue;
+                const int sw = n & 31;
+                const u32x2 lo = *(const u32x2*)(st + n * 256 + (((2 * k) ^ sw) * 8));
+                const u32x2 up = *(const u32x2*)(st + n * 256 + (((2 * k + 1) ^ sw) * 8));
+                const int b = m / o.S, s = m - b * o.S;
+                if (fast && m + 7 < M) {
+                    *(u32x4*)(o.vc + (((size_t)b * o.g + head) * 128 + n) * o.cap + s) =
+                        u32x4{lo[0], lo[1], up[0], up[1]};
+                } else {
+                    const uint32_t w4[4] = {lo[0], lo[1], up[0], up[1]};
+                    for (int e = 0; e < 8 && m + e < M; ++e) {
+                        int bb = b, ss = s + e;
+                        while (ss >= o.S) { ss -= o.S; ++bb; }
+                        o.vc[(((size_t)bb * o.g + head) * 128 + n) * o.cap + ss] =
+                            (bf16_t)(w4[e >> 1] >> (16 * (e & 1)));
                     }
                 }
             }
+            return;
+        }
+        // Q / K: 128 rows x 4 groups of 8 rotation pairs; 8 items per lane, their
+        // cos/sin rows (64 contiguous bytes each) requested before any is used.
+        int rowl[8], sp[8];
+        u32x4 cs[8][4];
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int id = lane + 64 * t;
+            rowl[t] = id >> 2;
+            const int m = min(mw + rowl[t], M - 1);
+            sp[t] = m % o.S;
+            const int c0 = 32 * pass + 8 * (id & 3);
+            const u32x4* tab = (const u32x4*)(o.rope + (size_t)sp[t] * 64 + c0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) cs[t][q] = tab[q];
+        }
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int id = lane + 64 * t, k = id & 3;
+            const int m = mw + rowl[t];
+            if (m >= M) continue;
+            const u32x4 a0 = ld_f32(st, rowl[t], 2 * k), a1 = ld_f32(st, rowl[t], 2 * k + 1);
+            const u32x4 b0 = ld_f32(st, rowl[t], 8 + 2 * k), b1 = ld_f32(st, rowl[t], 9 + 2 * k);
+            float x1[8], x2[8], c[8], sn[8];
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                x1[e] = __uint_as_float(a0[e]);
+                x1[e + 4] = __uint_as_float(a1[e]);
+                x2[e] = __uint_as_float(b0[e]);
+                x2[e + 4] = __uint_as_float(b1[e]);
+            }
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                c[e] = __uint_as_float(cs[t][e >> 1][2 * (e & 1)]);
+                sn[e] = __uint_as_float(cs[t][e >> 1][2 * (e & 1) + 1]);
+            }
+            u32x4 lo, up;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                lo[e] = pack2bf(x1[2 * e] * c[2 * e] - x2[2 * e] * sn[2 * e],
+                                x1[2 * e + 1] * c[2 * e + 1] - x2[2 * e + 1] * sn[2 * e + 1]);
+                up[e] = pack2bf(x2[2 * e] * c[2 * e] + x1[2 * e] * sn[2 * e],
+                                x2[2 * e + 1] * c[2 * e + 1] + x1[2 * e + 1] * sn[2 * e + 1]);
+            }
+            const int c0 = 32 * pass + 8 * k;
+            uint16_t* dst;
+            if (reg == 0) {
+                dst = o.q + (size_t)m * o.n_q + head * 128;
+            } else {
+                const int b = m / o.S;
+                dst = o.kc + (((size_t)b * o.g + head) * o.cap + sp[t]) * 128;
+            }
+            *(u32x4*)(dst + c0) = lo;
+            *(u32x4*)(dst + c0 + 64) = up;
+        }
     }
 };
 
+// Residual output y = x + acc, rounded once: the fp32 tile is staged in two passes of
+// 64 columns (128 x 64 fp32 = 32 KB per wave in 256-byte rows).
 struct ResidEpi {
+    static constexpr int kPasses = 2;
     const uint16_t* x;
     uint16_t* y;
-    __device__ __forceinline__ void operator()(f32x16 (&acc)[4][4], int mw, int nw, int lane, int M,
-                                               int N) const {
+    __device__ __forceinline__ void stage(int pass, f32x16 (&acc)[4][4], int mw, int nw, int lane,
+                                          int M, int N, char* st) const {
+        if (nw >= N) return;
         const int l32 = lane & 31, hi = lane >> 5;
 #pragma unroll
         for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                const int m = mw + 32 * mb + 8 * (i >> 2) + 4 * hi + (i & 3);
-                if (m >= M) continue;
-#pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
-                    const int n = nw + 32 * nb + l32;
-                    if (n < N) {
-                        const size_t off = (size_t)m * N + n;
-                        y[off] = f2bf(bf2f(x[off]) + acc[mb][nb][i]);
-                    }
-                }
+                const int m = 32 * mb + 8 * (i >> 2) + 4 * hi + (i & 3);
+                st_f32(st, m, l32, pass == 0 ? acc[mb][0][i] : acc[mb][2][i]);
+                st_f32(st, m, 32 + l32, pass == 0 ? acc[mb][1][i] : acc[mb][3][i]);
             }
     }
+    __device__ __forceinline__ void flush(int pass, int mw, int nw, int lane, int M, int N,
+                                          const char* st) const {
+        if (nw >= N) return;
+        // 16 items per lane (row, 8 columns); all residual loads are issued first.
+        u32x4 xv[16];
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+            const int ml = 8 * it + (lane >> 3), c8 = lane & 7;
+            const int m = min(mw + ml, M - 1);
+            xv[it] = *(const u32x4*)(x + (size_t)m * N + nw + 64 * pass + 8 * c8);
+        }
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+            const int ml = 8 * it + (lane >> 3), c8 = lane & 7;
+            const int m = mw + ml;
+            if (m >= M) continue;
+            const u32x4 p0 = ld_f32(st, ml, 2 * c8), p1 = ld_f32(st, ml, 2 * c8 + 1);
+            u32x4 out;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+                const float a0 = __uint_as_float(e < 2 ? p0[2 * e] : p1[2 * e - 4]);
+                const float a1 = __uint_as_float(e < 2 ? p0[2 * e + 1] : p1[2 * e - 3]);
+                const float x0 = __uint_as_float(xv[it][e] << 16);
+                const float x1 = __uint_as_float(xv[it][e] & 0xFFFF0000u);
+                out[e] = pack2bf(x0 + a0, x1 + a1);
+            }
+            *(u32x4*)(y + (size_t)m * N + nw + 64 * pass + 8 * c8) = out;
+        }
+    }
 };
+
+typedef __attribute__((address_space(1))) void gvoid_t;
+typedef __attribute__((address_space(3))) void lvoid_t;
+
+// LDS position of 16-byte chunk c of tile row r (rows are 128 B): spreads 16 consecutive
+// rows of one chunk column over all 64 banks.
+__device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
 template <class Epi>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict__ A, WRows W,
@@ -147,18 +262,28 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
     const int in_g = lid - group * GROUP_M * ntn;
     const int m0 = (first + in_g % gsz) * BM, n0 = (in_g / gsz) * BN;
 
-    // Loader: thread covers rows (tid >> 3) + 32 i of both tiles, 16-byte chunk tid & 7.
-    const int kc = tid & 7;
-    const u32x4* a_src[8];
-    const u32x4* w_src[8];
-    int soff[8];
+    // Direct global -> LDS loads: wave w fills tile rows 64 w .. 64 w + 63 of A and of W,
+    // eight 1 KB instructions each (8 rows of 128 B); lane l of instruction j covers row
+    // 64 w + 8 j + l / 8 and fetches the global chunk that belongs at LDS position l % 8.
+    const uint16_t* a_src[8];
+    const uint16_t* w_src[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        const int row = (tid >> 3) + 32 * i;
-        a_src[i] = (const u32x4*)(A + (size_t)min(m0 + row, M - 1) * K) + kc;
-        w_src[i] = (const u32x4*)w_row(W, min(n0 + row, N - 1), K) + kc;
-        soff[i] = row * 8 + (kc ^ (row & 7));
+    for (int j = 0; j < 8; ++j) {
+        const int row = 64 * wave + 8 * j + (lane >> 3);
+        const int c = swz(row, lane & 7);
+        a_src[j] = A + (size_t)min(m0 + row, M - 1) * K + 8 * c;
+        w_src[j] = w_row(W, min(n0 + row, N - 1), K) + 8 * c;
     }
+    auto issue = [&](int kt, int stg) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int r0 = 64 * wave + 8 * j;
+            __builtin_amdgcn_global_load_lds((gvoid_t*)(a_src[j] + kt * BK), (lvoid_t*)&lds[stg][0][r0 * 8],
+                                             16, 0, 0);
+            __builtin_amdgcn_global_load_lds((gvoid_t*)(w_src[j] + kt * BK), (lvoid_t*)&lds[stg][1][r0 * 8],
+                                             16, 0, 0);
+        }
+    };
 
     f32x16 acc[4][4];
 #pragma unroll
@@ -166,50 +291,37 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
 
-    u32x4 ra[8], rw[8];
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        ra[i] = a_src[i][0];
-        rw[i] = w_src[i][0];
-    }
-#pragma unroll
-    for (int i = 0; i < 8; ++i) {
-        lds[0][0][soff[i]] = ra[i];
-        lds[0][1][soff[i]] = rw[i];
-    }
-    __syncthreads();
-
     const int nk = K / BK;
     const int l32 = lane & 31, hi = lane >> 5;
-    // LDS offsets (in 16-byte chunks) of this lane's fragment rows; row & 7 == l32 & 7.
-    int a_off[4], b_off[4];
+    int a_off[4], b_off[4], rsw[4], bsw[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-        a_off[i] = (wm * 128 + 32 * i + l32) * 8;
-        b_off[i] = (wn * 128 + 32 * i + l32) * 8;
+        const int ra = wm * 128 + 32 * i + l32, rb = wn * 128 + 32 * i + l32;
+        a_off[i] = ra * 8;
+        b_off[i] = rb * 8;
+        rsw[i] = (ra >> 1) & 7;
+        bsw[i] = (rb >> 1) & 7;
     }
-    const int sw = l32 & 7;
     auto load_frags = [&](int stg, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
-        const int c = (2 * ks + hi) ^ sw;
+        const int c = 2 * ks + hi;
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-            fa[i] = as_bf16x8(lds[stg][0][a_off[i] + c]);
-            fb[i] = as_bf16x8(lds[stg][1][b_off[i] + c]);
+            fa[i] = as_bf16x8(lds[stg][0][a_off[i] + (c ^ rsw[i])]);
+            fb[i] = as_bf16x8(lds[stg][1][b_off[i] + (c ^ bsw[i])]);
         }
     };
+
+    issue(0, 0);
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
 
     bf16x8 fa[4], fb[4], ga[4], gb[4];
     load_frags(0, 0, fa, fb);
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt & 1;
         const bool more = kt + 1 < nk;
-        if (more) {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                ra[i] = a_src[i][(kt + 1) * 8];
-                rw[i] = w_src[i][(kt + 1) * 8];
-            }
-        }
+        // The other buffer was last read before the barrier that ended step kt - 1.
+        if (more) issue(kt + 1, cur ^ 1);
         // Four 16-wide k steps; the fragments of step ks + 1 are read from LDS while the
         // 16 MFMAs of step ks run (one ds_read slotted after each of the first 8 MFMAs).
 #pragma unroll
@@ -234,16 +346,20 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
             }
         }
         if (more) {
-#pragma unroll
-            for (int i = 0; i < 8; ++i) {
-                lds[cur ^ 1][0][soff[i]] = ra[i];
-                lds[cur ^ 1][1][soff[i]] = rw[i];
-            }
+            asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // this wave's part of tile kt + 1
+            __syncthreads();                                    // everyone's part, and tile kt read
+            load_frags(cur ^ 1, 0, fa, fb);
         }
-        __syncthreads();
-        if (more) load_frags(cur ^ 1, 0, fa, fb);
     }
-    epi(acc, m0 + wm * 128, n0 + wn * 128, lane, M, N);
+    // Epilogue through LDS, in Epi::kPasses passes over the wave's 32 KB.
+    char* st = (char*)&lds[0][0][0] + wave * 32768;
+#pragma unroll
+    for (int pass = 0; pass < Epi::kPasses; ++pass) {
+        __syncthreads();   // the LDS is free: last fragment reads / previous flush are done
+        epi.stage(pass, acc, m0 + wm * 128, n0 + wn * 128, lane, M, N, st);
+        __syncthreads();
+        epi.flush(pass, m0 + wm * 128, n0 + wn * 128, lane, M, N, st);
+    }
 }
 
 template <class Epi>
