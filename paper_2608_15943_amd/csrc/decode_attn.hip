@@ -125,7 +125,7 @@ __global__ __launch_bounds__(NT, 1) void decode_attn_kernel(
         const float mt = mx * scale_log2;
         if (__any(mt > m_run + kLazy)) {
             const float m_new = fmaxf(m_run, mt);
-            const float alpha = exp2f(m_run - m_new);
+            const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
             m_run = m_new;
             l_run *= alpha;
 #pragma unroll
@@ -139,7 +139,7 @@ __global__ __launch_bounds__(NT, 1) void decode_attn_kernel(
             for (int e = 0; e < 2; ++e)
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    p[4 * e + i] = exp2f(fmaf(sc[2 * s + e][i], scale_log2, -m_run));
+                    p[4 * e + i] = __builtin_amdgcn_exp2f(fmaf(sc[2 * s + e][i], scale_log2, -m_run));
                     l_run += p[4 * e + i];
                 }
             u32x4 w;

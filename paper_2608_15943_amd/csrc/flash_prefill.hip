@@ -21,7 +21,8 @@
 //   O^T[128 x 32] += V^T_tile P^T straight from the score registers.
 //   The lane that owns query q holds 32 of its 64 scores (the other 32 are in
 //   lane q ^ 32): the row max needs one exchange, the row sum none.
-// Online softmax in the exp2 domain with a lazily moved maximum: accumulators
+// Online softmax in the exp2 domain (raw v_exp_f32: arguments never exceed 8,
+// tiny results may flush to 0) with a lazily moved maximum: accumulators
 // are rescaled only when some row's maximum grows by more than 8 (a factor
 // 256), which keeps every exp2 argument <= 8.
 //
@@ -181,7 +182,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             const float mt = mx * scale_log2;                  // tile max, log2 domain
             if (__any(mt > m_run + kLazy)) {
                 const float m_new = fmaxf(m_run, mt);
-                const float alpha = exp2f(m_run - m_new);      // 0 on the first visible tile
+                const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);   // 0 on the first visible tile
                 m_run = m_new;
                 l_run *= alpha;
 #pragma unroll
@@ -195,7 +196,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                     float e[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        e[k] = exp2f(fmaf(s[mb][8 * p + k], scale_log2, -m_run));
+                        e[k] = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * p + k], scale_log2, -m_run));
                         l_run += e[k];
                     }
                     u32x4 w;
