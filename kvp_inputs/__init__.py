@@ -31,6 +31,7 @@ the rest.
 from __future__ import annotations
 
 import math
+import os
 from dataclasses import dataclass, field
 from typing import Dict, List, Optional, Sequence
 
@@ -56,16 +57,24 @@ KIND_LENS = 8     # ragged decode context lengths [B]
 KIND_XDEC = 9     # decode input activations [B, h]
 
 
+def _mix64_inplace(z: np.ndarray) -> np.ndarray:
+    """SplitMix64 finaliser applied in place to a uint64 array (wrapping arithmetic)."""
+    t = np.empty_like(z)
+    with np.errstate(over="ignore"):
+        np.right_shift(z, np.uint64(30), out=t)
+        z ^= t
+        z *= _M1
+        np.right_shift(z, np.uint64(27), out=t)
+        z ^= t
+        z *= _M2
+        np.right_shift(z, np.uint64(31), out=t)
+        z ^= t
+    return z
+
+
 def mix64(z: np.ndarray) -> np.ndarray:
     """SplitMix64 finaliser on a uint64 array (wrapping arithmetic)."""
-    z = np.asarray(z, dtype=np.uint64).copy()
-    with np.errstate(over="ignore"):
-        z ^= z >> np.uint64(30)
-        z *= _M1
-        z ^= z >> np.uint64(27)
-        z *= _M2
-        z ^= z >> np.uint64(31)
-    return z
+    return _mix64_inplace(np.array(z, dtype=np.uint64, copy=True))
 
 
 def tensor_id(kind: int, layer: int = 0) -> int:
@@ -81,10 +90,12 @@ def stream_key(seed: int, tid: int) -> int:
 
 def raw64(key: int, idx: np.ndarray) -> np.ndarray:
     """Output idx+1 of the SplitMix64 stream with state ``key``."""
-    idx = np.asarray(idx, dtype=np.uint64)
+    z = np.array(idx, dtype=np.uint64, copy=True)
     with np.errstate(over="ignore"):
-        z = np.uint64(key) + (idx + np.uint64(1)) * GAMMA
-    return mix64(z)
+        z += np.uint64(1)
+        z *= GAMMA
+        z += np.uint64(key)
+    return _mix64_inplace(z)
 
 
 def normal_scale(sigma: float) -> np.float32:
@@ -92,20 +103,53 @@ def normal_scale(sigma: float) -> np.float32:
     return np.float32(float(sigma) * math.sqrt(3.0) / 65536.0)
 
 
-def normal_f32(key: int, idx: np.ndarray, sigma: float) -> np.ndarray:
+def _normal_chunk(key: int, idx: np.ndarray, scale: np.float32, bf16: bool = False) -> np.ndarray:
     h = raw64(key, idx)
-    s = (h & _U16) + ((h >> np.uint64(16)) & _U16) + \
-        ((h >> np.uint64(32)) & _U16) + ((h >> np.uint64(48)) & _U16)
-    znum = s.astype(np.int64) - 131070
-    return znum.astype(np.float32) * normal_scale(sigma)
+    s = (h & _U16).astype(np.int32)
+    h >>= np.uint64(16)
+    s += (h & _U16).astype(np.int32)
+    h >>= np.uint64(16)
+    s += (h & _U16).astype(np.int32)
+    h >>= np.uint64(16)
+    s += h.astype(np.int32)
+    s -= 131070
+    v = s.astype(np.float32) * scale
+    return round_to_bf16(v) if bf16 else v
+
+
+_CHUNK = 1 << 22
+
+
+def normal_f32(key: int, idx: np.ndarray, sigma: float, bf16: bool = False) -> np.ndarray:
+    """Irwin-Hall(4) normals at logical indices idx (any shape), optionally rounded to
+    bf16 (returned as fp32); large inputs are split over threads."""
+    idx = np.asarray(idx, dtype=np.uint64)
+    scale = normal_scale(sigma)
+    flat = idx.reshape(-1)
+    n = flat.size
+    if n <= _CHUNK:
+        return _normal_chunk(key, flat, scale, bf16).reshape(idx.shape)
+    out = np.empty(n, dtype=np.float32)
+
+    def work(lo):
+        hi = min(lo + _CHUNK, n)
+        out[lo:hi] = _normal_chunk(key, flat[lo:hi], scale, bf16)
+
+    import concurrent.futures as cf
+    workers = max(1, min(16, os.cpu_count() or 1))
+    with cf.ThreadPoolExecutor(workers) as ex:
+        list(ex.map(work, range(0, n, _CHUNK)))
+    return out.reshape(idx.shape)
 
 
 def f32_to_bf16_bits(x: np.ndarray) -> np.ndarray:
-    """Round fp32 to bf16 (nearest-even) and return the 16-bit patterns."""
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    lsb = (u >> np.uint64(16)) & np.uint64(1)
-    r = (u + np.uint64(0x7FFF) + lsb) >> np.uint64(16)
-    return r.astype(np.uint16)
+    """Round finite fp32 to bf16 (nearest-even) and return the 16-bit patterns."""
+    u = np.array(x, dtype=np.float32, copy=True).view(np.uint32)
+    lsb = (u >> np.uint32(16)) & np.uint32(1)
+    u += np.uint32(0x7FFF)          # finite inputs stay below 2**32
+    u += lsb
+    u >>= np.uint32(16)
+    return u.astype(np.uint16)
 
 
 def bf16_bits_to_f32(b: np.ndarray) -> np.ndarray:
@@ -119,12 +163,9 @@ def round_to_bf16(x: np.ndarray) -> np.ndarray:
 
 def normal_values(seed: int, tid: int, idx: np.ndarray, sigma: float, dtype: str) -> np.ndarray:
     """Synthetic values at logical indices ``idx`` as fp32 (bf16-exact if dtype='bf16')."""
-    v = normal_f32(stream_key(seed, tid), idx, sigma)
-    if dtype == "bf16":
-        v = round_to_bf16(v)
-    elif dtype != "fp32":
+    if dtype not in ("bf16", "fp32"):
         raise ValueError(f"unknown dtype {dtype!r}")
-    return v
+    return normal_f32(stream_key(seed, tid), idx, sigma, bf16=(dtype == "bf16"))
 
 
 # ---------------------------------------------------------------------------

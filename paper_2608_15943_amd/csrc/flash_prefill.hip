@@ -152,14 +152,16 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             }
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
+                // Fences keep the reads of step ks + 2 ahead of the MFMAs of step ks (left to
+                // itself the scheduler sinks each read next to its use and waits on it).
                 if (ks + 2 < 8) {
                     kf[(ks + 2) % 3][0] = kfrag(0, ks + 2);
                     kf[(ks + 2) % 3][1] = kfrag(1, ks + 2);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 2, 0);   // 2 LDS reads, then
                 }
+                __builtin_amdgcn_sched_barrier(0);
                 s[0] = mfma32x32x16(kf[ks % 3][0], qf[ks], s[0]);
                 s[1] = mfma32x32x16(kf[ks % 3][1], qf[ks], s[1]);
-                __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);       // 2 MFMAs
+                __builtin_amdgcn_sched_barrier(0);
             }
             // Register i of block mb holds position t0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
             const bool diag = (t0 + BKV - 1 > q0w) || (t0 + BKV > S);
@@ -217,13 +219,11 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             for (int i = 0; i < 3; ++i) vf[i] = vfrag(i);
 #pragma unroll
             for (int i = 0; i < 16; ++i) {
-                if (i + 3 < 16) {
-                    vf[(i + 3) & 3] = vfrag(i + 3);
-                    __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-                }
+                if (i + 3 < 16) vf[(i + 3) & 3] = vfrag(i + 3);
+                __builtin_amdgcn_sched_barrier(0);
                 const int db = i >> 2, mb = (i >> 1) & 1, p = i & 1;
                 o[db] = mfma32x32x16(vf[i & 3], pb[mb][p], o[db]);
-                __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+                __builtin_amdgcn_sched_barrier(0);
             }
         }
         // One barrier: tile t + 1 has landed in LDS (every wave waited for its own loads)

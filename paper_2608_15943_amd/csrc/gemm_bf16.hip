@@ -8,7 +8,8 @@
 //     sits in the same lane, 64 columns on), then Q goes to its buffer, K to
 //     the producer's cache slot and V, transposed, to the V slot.  A consumer
 //     runs the same kernel with N = a * d_h (Q only).
-//   * residual: X_{l+1} = X_l + O W_O^T.
+//   * residual: X_{l+1} = X_l + O W_O^T, with the residual stream read and
+//     written in fp32 between layers and a bf16 copy for the next projection.
 //
 // Tiling: 256 x 256 x 64 per workgroup of 4 waves (2 x 2, 128 x 128 each, a
 // 4 x 4 grid of 32 x 32 MFMA blocks = 256 fp32 accumulators per lane).
@@ -190,12 +191,16 @@ struct QkvEpi {
     }
 };
 
-// Residual output y = x + acc, rounded once: the fp32 tile is staged in two passes of
-// 64 columns (128 x 64 fp32 = 32 KB per wave in 256-byte rows).
+// Residual update y = x + acc.  x is the bf16 layer input (XF32 = false) or the fp32
+// residual stream (XF32 = true, updated in place through yf); y is written in bf16,
+// yf (optional) in fp32.  The fp32 tile is staged in two passes of 64 columns
+// (128 x 64 fp32 = 32 KB per wave in 256-byte rows).
+template <bool XF32>
 struct ResidEpi {
     static constexpr int kPasses = 2;
-    const uint16_t* x;
+    const void* x;
     uint16_t* y;
+    float* yf;
     __device__ __forceinline__ void stage(int pass, f32x16 (&acc)[4][4], int mw, int nw, int lane,
                                           int M, int N, char* st) const {
         if (nw >= N) return;
@@ -213,12 +218,17 @@ struct ResidEpi {
                                           const char* st) const {
         if (nw >= N) return;
         // 16 items per lane (row, 8 columns); all residual loads are issued first.
-        u32x4 xv[16];
+        u32x4 xv[16][XF32 ? 2 : 1];
 #pragma unroll
         for (int it = 0; it < 16; ++it) {
             const int ml = 8 * it + (lane >> 3), c8 = lane & 7;
-            const int m = min(mw + ml, M - 1);
-            xv[it] = *(const u32x4*)(x + (size_t)m * N + nw + 64 * pass + 8 * c8);
+            const size_t off = (size_t)min(mw + ml, M - 1) * N + nw + 64 * pass + 8 * c8;
+            if (XF32) {
+                xv[it][0] = *(const u32x4*)((const float*)x + off);
+                xv[it][XF32 ? 1 : 0] = *(const u32x4*)((const float*)x + off + 4);
+            } else {
+                xv[it][0] = *(const u32x4*)((const uint16_t*)x + off);
+            }
         }
 #pragma unroll
         for (int it = 0; it < 16; ++it) {
@@ -226,16 +236,33 @@ struct ResidEpi {
             const int m = mw + ml;
             if (m >= M) continue;
             const u32x4 p0 = ld_f32(st, ml, 2 * c8), p1 = ld_f32(st, ml, 2 * c8 + 1);
-            u32x4 out;
+            float r[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
-                const float a0 = __uint_as_float(e < 2 ? p0[2 * e] : p1[2 * e - 4]);
-                const float a1 = __uint_as_float(e < 2 ? p0[2 * e + 1] : p1[2 * e - 3]);
-                const float x0 = __uint_as_float(xv[it][e] << 16);
-                const float x1 = __uint_as_float(xv[it][e] & 0xFFFF0000u);
-                out[e] = pack2bf(x0 + a0, x1 + a1);
+                const float a0 = __uint_as_float(p0[e]), a1 = __uint_as_float(p1[e]);
+                float x0, x1;
+                if (XF32) {
+                    x0 = __uint_as_float(xv[it][0][e]);
+                    x1 = __uint_as_float(xv[it][XF32 ? 1 : 0][e]);
+                } else {
+                    const uint32_t w0 = xv[it][0][e >> 1], w1 = xv[it][0][2 + (e >> 1)];
+                    x0 = __uint_as_float((e & 1) ? (w0 & 0xFFFF0000u) : (w0 << 16));
+                    x1 = __uint_as_float((e & 1) ? (w1 & 0xFFFF0000u) : (w1 << 16));
+                }
+                r[e] = x0 + a0;
+                r[4 + e] = x1 + a1;
             }
-            *(u32x4*)(y + (size_t)m * N + nw + 64 * pass + 8 * c8) = out;
+            const size_t off = (size_t)m * N + nw + 64 * pass + 8 * c8;
+            u32x4 out;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) out[e] = pack2bf(r[2 * e], r[2 * e + 1]);
+            *(u32x4*)(y + off) = out;
+            if (yf) {
+                *(u32x4*)(yf + off) = u32x4{__float_as_uint(r[0]), __float_as_uint(r[1]),
+                                            __float_as_uint(r[2]), __float_as_uint(r[3])};
+                *(u32x4*)(yf + off + 4) = u32x4{__float_as_uint(r[4]), __float_as_uint(r[5]),
+                                                __float_as_uint(r[6]), __float_as_uint(r[7])};
+            }
         }
     }
 };
@@ -377,10 +404,11 @@ hipError_t gemm_qkv_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
     return launch(x, w, M, N, K, QkvEpi{o}, st);
 }
 
-hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const uint16_t* x_res,
-                           uint16_t* y, int M, int N, int K, hipStream_t st) {
+hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_res, bool x_f32,
+                           uint16_t* y, float* yf, int M, int N, int K, hipStream_t st) {
     WRows W{{w, nullptr, nullptr}, {N, 0, 0}};
-    return launch(a, W, M, N, K, ResidEpi{x_res, y}, st);
+    if (x_f32) return launch(a, W, M, N, K, ResidEpi<true>{x_res, y, yf}, st);
+    return launch(a, W, M, N, K, ResidEpi<false>{x_res, y, yf}, st);
 }
 
 }  // namespace kvp

@@ -29,9 +29,10 @@ struct QkvOut {
 hipError_t gemm_qkv_bf16(const uint16_t* x, const WRows& w, int M, int N, int K, const QkvOut& o,
                          hipStream_t st);
 
-// y = x_res + a @ w^T, a [M][K], w [N][K], x_res, y [M][N].
-hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const uint16_t* x_res,
-                           uint16_t* y, int M, int N, int K, hipStream_t st);
+// y = x_res + a @ w^T, a [M][K], w [N][K]; x_res [M][N] in bf16 or (x_f32) fp32;
+// y [M][N] bf16 and, if yf != nullptr, yf [M][N] fp32 (may alias an fp32 x_res).
+hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_res, bool x_f32,
+                           uint16_t* y, float* yf, int M, int N, int K, hipStream_t st);
 
 // Causal flash attention: q [B*S][a*128], K/V slots of the producer, o [B*S][a*128].
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
@@ -39,9 +40,11 @@ hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint1
 
 // ---- bf16 decode ------------------------------------------------------------
 
-// out_f32 [M][N] = x @ w^T (M <= 64), or (resid) y = x_res + x @ w^T in bf16.
+// out_f32 [M][N] = x @ w^T (M <= 64), or (out_f32 == nullptr) the residual update
+// y = x_res + x @ w^T with x_res in bf16 or (x_f32) fp32, y in bf16 and yf (optional) fp32.
 hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
-                            float* out_f32, const uint16_t* x_res, uint16_t* y, hipStream_t st);
+                            float* out_f32, const void* x_res, bool x_f32, uint16_t* y, float* yf,
+                            hipStream_t st);
 
 // Split-K attention of one new query per sequence over positions [0, len_b].
 hipError_t decode_attn_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,

@@ -53,7 +53,17 @@ size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 struct Workspace {
-    size_t q = 0, o = 0, x = 0, rope = 0, proj = 0, part = 0, total = 0;
+    size_t q = 0, o = 0, xb = 0, xr = 0, rope = 0, proj = 0, part = 0, total = 0;
+};
+
+// Where one layer reads and writes.  The residual stream between layers is fp32 (xr,
+// updated in place); bf16 models feed the matrix cores a bf16 copy of it (xb).
+struct LayerIO {
+    const void* a;     // projection input [rows][h], model dtype
+    const void* res;   // residual source [rows][h]
+    bool res_f32;      // res is fp32 (otherwise the model dtype)
+    void* y;           // output [rows][h], model dtype
+    float* yf;         // optional fp32 copy of the output (bf16 models)
 };
 
 }  // namespace
@@ -97,7 +107,8 @@ Workspace layout(const kvp_ctx& c, int phase, int B, int S) {
     const size_t nproj = (size_t)(c.d.a + 2 * c.d.g) * c.d.d_h;
     w.q = take(rows * c.n_q() * e);
     w.o = take(rows * c.n_q() * e);
-    w.x = take(rows * c.d.h * e);
+    w.xb = take(rows * c.d.h * e);
+    w.xr = take(rows * c.d.h * sizeof(float));
     if (phase == KVP_PHASE_PREFILL) {
         if (c.bf16())
             w.rope = take((size_t)S * (c.d.d_h / 2) * sizeof(float2));
@@ -112,6 +123,28 @@ Workspace layout(const kvp_ctx& c, int phase, int B, int S) {
     }
     w.total = off;
     return w;
+}
+
+// The l-th layer's IO within a stack of L layers: layer 0 reads the caller's x, the last
+// writes the caller's y; in between the fp32 residual stream xr is updated in place and
+// (bf16 models) its bf16 copy xb feeds the next projection.
+LayerIO stack_io(bool bf16, int l, int L, const void* x, void* y, char* ws, const Workspace& w) {
+    LayerIO io;
+    float* xr = (float*)(ws + w.xr);
+    if (bf16) {
+        io.a = l == 0 ? x : (const void*)(ws + w.xb);
+        io.res = l == 0 ? x : (const void*)xr;
+        io.res_f32 = l != 0;
+        io.y = l == L - 1 ? y : (void*)(ws + w.xb);
+        io.yf = l == L - 1 ? nullptr : xr;
+    } else {
+        io.a = l == 0 ? x : (const void*)xr;
+        io.res = io.a;
+        io.res_f32 = true;
+        io.y = l == L - 1 ? y : (void*)xr;
+        io.yf = nullptr;
+    }
+    return io;
 }
 
 int check_hip(hipError_t e, const char* what) {
@@ -170,8 +203,9 @@ kvp::WRows proj_rows(const kvp_ctx* c, int l, bool producer) {
     return w;
 }
 
-// One prefill layer: x_in [B*S, h] -> y_out, attention output into o_buf.
-int run_prefill_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, void* o_buf, char* ws,
+// One prefill layer over rows [B*S]: io.a -> projections, io.res + O W_O^T -> io.y
+// (and io.yf), attention output into o_buf.
+int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* ws,
                       const Workspace& w, int B, int S, hipStream_t st) {
     const int p = c->tau[l];
     const bool producer = p == l;
@@ -195,7 +229,7 @@ int run_prefill_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, void* o_
         qo.cap = c->d.kv_capacity;
         qo.S = S;
         if ((rc = timed(c, KVP_K_QKV_GEMM, st, [&] {
-                 return check_hip(kvp::gemm_qkv_bf16((const uint16_t*)x_in, wr, M, N, h, qo, st),
+                 return check_hip(kvp::gemm_qkv_bf16((const uint16_t*)io.a, wr, M, N, h, qo, st),
                                   "projection GEMM");
              })))
             return rc;
@@ -208,14 +242,15 @@ int run_prefill_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, void* o_
             return rc;
         return timed(c, KVP_K_OPROJ_GEMM, st, [&] {
             return check_hip(kvp::gemm_resid_bf16((const uint16_t*)o_buf, (const uint16_t*)wo.p[0],
-                                                  (const uint16_t*)x_in, (uint16_t*)y_out, M, h, nq, st),
+                                                  io.res, io.res_f32, (uint16_t*)io.y, io.yf, M, h,
+                                                  nq, st),
                              "output projection");
         });
     }
     float* proj = (float*)(ws + w.proj);
     float* q = (float*)(ws + w.q);
     if ((rc = timed(c, KVP_K_QKV_GEMM, st, [&] {
-             return check_hip(kvp::gemm_f32((const float*)x_in, wr, M, N, h, proj, nullptr, st),
+             return check_hip(kvp::gemm_f32((const float*)io.a, wr, M, N, h, proj, nullptr, st),
                               "projection GEMM (fp32)");
          })))
         return rc;
@@ -235,8 +270,8 @@ int run_prefill_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, void* o_
          })))
         return rc;
     return timed(c, KVP_K_OPROJ_GEMM, st, [&] {
-        return check_hip(kvp::gemm_f32((const float*)o_buf, wo, M, h, nq, (float*)y_out,
-                                       (const float*)x_in, st),
+        return check_hip(kvp::gemm_f32((const float*)o_buf, wo, M, h, nq, (float*)io.y,
+                                       (const float*)io.res, st),
                          "output projection (fp32)");
     });
 }
@@ -251,7 +286,7 @@ int choose_split(const kvp_ctx* c, int B, int max_len, int* nsplit) {
     return split;
 }
 
-int run_decode_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, const int32_t* lens,
+int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
                      int max_len, char* ws, const Workspace& w, int B, hipStream_t st) {
     const int p = c->tau[l];
     const bool producer = p == l;
@@ -268,10 +303,10 @@ int run_decode_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, const int
     int rc;
     if ((rc = timed(c, KVP_K_DEC_GEMM, st, [&] {
              return c->bf16()
-                        ? check_hip(kvp::gemm_skinny_bf16((const uint16_t*)x_in, wr, B, N, h, proj,
-                                                          nullptr, nullptr, st),
+                        ? check_hip(kvp::gemm_skinny_bf16((const uint16_t*)io.a, wr, B, N, h, proj,
+                                                          nullptr, false, nullptr, nullptr, st),
                                     "decode projection GEMM")
-                        : check_hip(kvp::gemm_f32((const float*)x_in, wr, B, N, h, proj, nullptr, st),
+                        : check_hip(kvp::gemm_f32((const float*)io.a, wr, B, N, h, proj, nullptr, st),
                                     "decode projection GEMM (fp32)");
          })))
         return rc;
@@ -301,8 +336,8 @@ int run_decode_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, const int
              })))
             return rc;
         return timed(c, KVP_K_DEC_OPROJ, st, [&] {
-            return check_hip(kvp::gemm_skinny_bf16((const uint16_t*)o, wo, B, h, nq, nullptr,
-                                                   (const uint16_t*)x_in, (uint16_t*)y_out, st),
+            return check_hip(kvp::gemm_skinny_bf16((const uint16_t*)o, wo, B, h, nq, nullptr, io.res,
+                                                   io.res_f32, (uint16_t*)io.y, io.yf, st),
                              "decode output projection");
         });
     }
@@ -314,7 +349,7 @@ int run_decode_layer(kvp_ctx* c, int l, const void* x_in, void* y_out, const int
          })))
         return rc;
     return timed(c, KVP_K_DEC_OPROJ, st, [&] {
-        return check_hip(kvp::gemm_f32((const float*)o, wo, B, h, nq, (float*)y_out, (const float*)x_in,
+        return check_hip(kvp::gemm_f32((const float*)o, wo, B, h, nq, (float*)io.y, (const float*)io.res,
                                        st),
                          "decode output projection (fp32)");
     });
@@ -506,13 +541,10 @@ extern "C" int kvp_prefill(kvp_ctx* ctx, const void* x, void* y, int B, int S, v
                                              "RoPE table");
                         })))
         return rc;
-    void* bufs[2] = {y, base + w.x};   // the last layer writes y
     const int L = ctx->d.L;
-    const void* cur = x;
     for (int l = 0; l < L; ++l) {
-        void* out = bufs[(L - 1 - l) & 1];
-        if ((rc = run_prefill_layer(ctx, l, cur, out, base + w.o, base, w, B, S, st))) return rc;
-        cur = out;
+        const LayerIO io = stack_io(ctx->bf16(), l, L, x, y, base, w);
+        if ((rc = run_prefill_layer(ctx, l, io, base + w.o, base, w, B, S, st))) return rc;
     }
     return ok();
 }
@@ -534,7 +566,8 @@ extern "C" int kvp_layer_forward(kvp_ctx* ctx, int l, const void* x, void* attn_
                                              "RoPE table");
                         })))
         return rc;
-    return run_prefill_layer(ctx, l, x, y, attn_out ? attn_out : base + w.o, base, w, B, S, st);
+    LayerIO io{x, x, !ctx->bf16(), y, nullptr};
+    return run_prefill_layer(ctx, l, io, attn_out ? attn_out : base + w.o, base, w, B, S, st);
 }
 
 extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
@@ -557,13 +590,10 @@ extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_d
     if ((rc = check_layers(ctx, 0, ctx->d.L))) return rc;
     hipStream_t st = (hipStream_t)stream;
     char* base = (char*)ws;
-    void* bufs[2] = {y, base + w.x};
     const int L = ctx->d.L;
-    const void* cur = x;
     for (int l = 0; l < L; ++l) {
-        void* out = bufs[(L - 1 - l) & 1];
-        if ((rc = run_decode_layer(ctx, l, cur, out, len_dev, max_len, base, w, B, st))) return rc;
-        cur = out;
+        const LayerIO io = stack_io(ctx->bf16(), l, L, x, y, base, w);
+        if ((rc = run_decode_layer(ctx, l, io, len_dev, max_len, base, w, B, st))) return rc;
     }
     return ok();
 }

@@ -100,7 +100,7 @@ constexpr int SK_THREADS = 256;
 
 __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(
     const uint16_t* __restrict__ X, WRows W, int M, int N, int K, float* __restrict__ out,
-    const uint16_t* __restrict__ xres, uint16_t* __restrict__ y) {
+    const void* xres, int xres_f32, uint16_t* __restrict__ y, float* yf) {
     __shared__ f32x4 red[4][4][64];   // [wave][m block][lane]
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     const int col = lane & 15, grp = lane >> 4;
@@ -145,10 +145,14 @@ __global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(
             const int m = 16 * mb + 4 * grp + i;
             if (m < M && n < N) {
                 const size_t off = (size_t)m * N + n;
-                if (out)
+                if (out) {
                     out[off] = v[i];
-                else
-                    y[off] = f2bf(bf2f(xres[off]) + v[i]);
+                } else {
+                    const float r = (xres_f32 ? ((const float*)xres)[off]
+                                              : bf2f(((const uint16_t*)xres)[off])) + v[i];
+                    y[off] = f2bf(r);
+                    if (yf) yf[off] = r;
+                }
             }
         }
     }
@@ -270,9 +274,10 @@ hipError_t rope_scatter(const float* proj, int rows, int S, const int32_t* lens,
 }
 
 hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
-                            float* out_f32, const uint16_t* x_res, uint16_t* y, hipStream_t st) {
+                            float* out_f32, const void* x_res, bool x_f32, uint16_t* y, float* yf,
+                            hipStream_t st) {
     hipLaunchKernelGGL(gemm_skinny_kernel, dim3((N + 15) / 16), dim3(SK_THREADS), 0, st, x, w, M, N, K,
-                       out_f32, x_res, y);
+                       out_f32, x_res, x_f32 ? 1 : 0, y, yf);
     return hipGetLastError();
 }
 
