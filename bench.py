@@ -80,7 +80,12 @@ def decode_bytes(w: ki.Workload, lens, tau=None):
 # ---------------------------------------------------------------------------
 
 class Stack:
-    def __init__(self, w: ki.Workload, B: int, max_seq: int, cap: int, fill_npos: int = 0):
+    """Weights and KV slots of a workload on the device.  alias_of maps a producer to an
+    earlier producer whose slot memory it reuses (used only when the unshared map does
+    not fit in HBM; timing is unaffected because every slot is far larger than the caches)."""
+
+    def __init__(self, w: ki.Workload, B: int, max_seq: int, cap: int, fill_npos: int = 0,
+                 alias_of=None):
         import torch
         from kvp_inputs import device as kd
         from paper_2608_15943_amd import binding as kb
@@ -102,10 +107,13 @@ class Stack:
             self.model.kvp_set_layer(l, t["wq"].data_ptr(), t["wk"].data_ptr() if prod else 0,
                                      t["wv"].data_ptr() if prod else 0, t["wo"].data_ptr())
             if prod:
-                K = torch.empty((B, w.g, cap, w.d_h), dtype=dt, device="cuda")
-                V = torch.empty((B, w.g, w.d_h, cap), dtype=dt, device="cuda")
-                if fill_npos:
-                    kd.fill_cache(w, l, K.data_ptr(), V.data_ptr(), B, cap, fill_npos)
+                if alias_of and l in alias_of:
+                    K, V = self.keep[alias_of[l]]["K"], self.keep[alias_of[l]]["V"]
+                else:
+                    K = torch.empty((B, w.g, cap, w.d_h), dtype=dt, device="cuda")
+                    V = torch.empty((B, w.g, w.d_h, cap), dtype=dt, device="cuda")
+                    if fill_npos:
+                        kd.fill_cache(w, l, K.data_ptr(), V.data_ptr(), B, cap, fill_npos)
                 self.model.kvp_set_kv_slot(l, K.data_ptr(), V.data_ptr())
                 t["K"], t["V"] = K, V
             self.keep.append(t)
@@ -154,7 +162,7 @@ def bench_prefill(w: ki.Workload, steps: int, warmup: int, tau=None):
     return ms, prof, ok
 
 
-def bench_decode(w: ki.Workload, steps: int, warmup: int):
+def bench_decode(w: ki.Workload, steps: int, warmup: int, alias_of=None):
     import torch
     from kvp_inputs import device as kd
     from paper_2608_15943_amd import binding as kb
@@ -162,7 +170,7 @@ def bench_decode(w: ki.Workload, steps: int, warmup: int):
     B = w.batch
     max_len = int(lens.max())
     t0 = time.perf_counter()
-    st = Stack(w, B, 1, w.kv_capacity, fill_npos=max_len)
+    st = Stack(w, B, 1, w.kv_capacity, fill_npos=max_len, alias_of=alias_of)
     log(f"[bench] decode setup {time.perf_counter() - t0:.1f}s "
         f"({torch.cuda.memory_allocated() / 2**30:.1f} GiB resident)")
     x = torch.empty((B, w.h), dtype=torch.bfloat16, device="cuda")
@@ -209,8 +217,59 @@ def cpu_baseline(w: ki.Workload, s_sample: int):
     flops = sum(prefill_flops(w, 1, s_sample).values())
     return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
             "kind": "oracle",
-            "sample": f"sequence 0 of 4, first {s_sample} positions (causal prefix, exact), "
-                      f"all {w.L} layers, fp64 NumPy; {dt:.1f} s"}
+            "sample": (f"sequence 0 of {w.batch}, " +
+                       (f"all {s_sample} positions" if s_sample == w.seq else
+                        f"first {s_sample} positions (causal prefix, exact)") +
+                       f", all {w.L} layers, fp64 NumPy with host BLAS; {dt:.1f} s")}
+
+
+def calibrate_copy():
+    """A plain device-to-device copy of exactly 1 GiB, five times: rocprofv3's FETCH_SIZE and
+    WRITE_SIZE for this kernel give the factor between the counters and true bytes."""
+    import torch
+    n = 1 << 30
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 5}))
+
+
+def roofline_entry(kernel, prof, per_unit, units_per_launch, peak, unit, bound):
+    """Algorithmic work per launch (per-unit figure x units one launch processes) over the
+    kernel's average launch time, measured with HIP events on the launch stream."""
+    n, t = prof[kernel]
+    per_launch = per_unit * units_per_launch
+    achieved = per_launch / (t / n * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
+    return {"bound": bound, "kernel": kernel, "achieved": round(achieved, 2), "peak": peak,
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel),
+            "work_per_launch": per_launch, "avg_launch_ms": round(t / n, 5)}
+
+
+def traffic_for(kernel):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE counter runs (scaled by
+    the factor a plain copy of known size gives), or None once the kernel's sources differ
+    from the ones the counters were taken on."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        ent = json.load(f).get(kernel)
+    if not ent:
+        return None
+    h = hashlib.sha1()
+    for rel in ent["sources"]:
+        src = os.path.join(ROOT, rel)
+        if not os.path.exists(src):
+            return None
+        with open(src, "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != ent["sources_sha1"]:
+        return None
+    return ent["bytes_per_launch"]
 
 
 def main():
@@ -221,8 +280,15 @@ def main():
     ap.add_argument("--no-decode", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-unshared", action="store_true")
-    ap.add_argument("--cpu-seq", type=int, default=2048)
+    ap.add_argument("--cpu-seq", type=int, default=4096)
+    ap.add_argument("--no-extra", action="store_true",
+                    help="skip the 70B-shaped prefill and the ragged 128K decode lines")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the KV-shared block is measured on one GPU's share; "
               f"see DESIGN.md for how it shards); --gpus {args.gpus} is not supported", file=sys.stderr)
@@ -243,13 +309,10 @@ def main():
     value = total / (ms * 1e-3) / 1e12
     kernels = {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof.items()}
     dom = max(("qkv_gemm", "flash_attn", "oproj_gemm"), key=lambda k: prof.get(k, (0, 0.0))[1])
-    n_l, t_l = prof[dom]
-    per_launch = flops[dom] * args.steps / n_l          # algorithmic FLOPs per launch
-    achieved = per_launch / (t_l / n_l * 1e-3) / 1e12
-    roofline = {"bound": "mfma", "kernel": dom, "achieved": round(achieved, 2),
-                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(achieved / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                "flops_per_launch": per_launch, "avg_launch_ms": round(t_l / n_l, 5)}
+    n_l = prof[dom][0]
+    roofline = roofline_entry(dom, prof, flops[dom] / w.L, w.L * args.steps / n_l,
+                              PEAK_BF16_TFLOPS, "TFLOP/s", "mfma")
+    roofline["per_unit"] = "algorithmic FLOPs of one layer of the stack (batch 4 x 4096 tokens)"
     log(f"[bench] prefill {ms:.3f} ms/step, {value:.1f} TFLOP/s; kernels {kernels}")
 
     result = {
@@ -263,6 +326,8 @@ def main():
                    "causal": True, "map": w.tau, "parallelism": "none (1 GPU)"},
         "roofline": roofline,
         "kernels": kernels,
+        "per_kernel_tflops": {k: round(flops[k] * args.steps / prof[k][1] / 1e9, 1)
+                              for k in flops if k in prof},
         "finite": finite,
     }
 
@@ -275,35 +340,95 @@ def main():
                                         "unshared_ms_per_step": round(ms_u, 4)}
         log(f"[bench] identity map {ms_u:.3f} ms/step (speedup {ms_u / ms:.4f}, ideal {ideal:.4f})")
 
+    if not args.no_extra:
+        result["prefill_70b_stage"] = bench_70b(args.steps, args.warmup)
+
     if not args.no_decode:
+        steps_d, warm_d = max(3, args.steps // 2), max(1, args.warmup // 2)
         wd = ki.decode_32k()
-        log(f"[bench] decode {wd.name}")
-        dms, dprof, dfin, lens = bench_decode(wd, max(3, args.steps // 2), max(1, args.warmup // 2))
-        db = decode_bytes(wd, lens)
-        dtotal = sum(db.values())
-        n_a, t_a = dprof["dec_attn"]
-        steps_d = max(3, args.steps // 2)
-        att_launch = db["dec_attn"] * steps_d / n_a
-        att_gbs = att_launch / (t_a / n_a * 1e-3) / 1e9
-        result["decode"] = {
-            "workload": wd.name, "tokens_per_s": round(wd.batch / (dms * 1e-3), 2),
-            "ms_per_step": round(dms, 4), "hbm_gbs": round(dtotal / (dms * 1e-3) / 1e9, 1),
-            "hbm_frac": round(dtotal / (dms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "bytes_per_step": dtotal, "finite": dfin,
-            "roofline": {"bound": "hbm", "kernel": "dec_attn", "achieved": round(att_gbs, 1),
-                         "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                         "frac": round(att_gbs / PEAK_HBM_GBS, 4), "traffic": None,
-                         "bytes_per_launch": att_launch, "avg_launch_ms": round(t_a / n_a, 5)},
-            "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in dprof.items()},
-        }
-        log(f"[bench] decode {dms:.3f} ms/step, {wd.batch / (dms * 1e-3):.1f} tok/s, "
-            f"attention {att_gbs:.0f} GB/s")
+        result["decode"] = decode_entry(wd, steps_d, warm_d)
+        if not args.no_unshared:
+            # Identity map: every layer owns a cache.  All 32 caches (275 GB) do not fit
+            # beside the rest, so former consumers reuse their former producer's memory;
+            # every layer still reads and appends its own full cache.
+            wi = wd.with_map(list(range(wd.L)), "-identity")
+            u = decode_entry(wi, steps_d, warm_d, alias_of={l: wd.tau[l] for l in range(wd.L)
+                                                            if wd.tau[l] != l})
+            result["decode"]["shared_vs_unshared"] = {
+                "step_speedup": round(u["ms_per_step"] / result["decode"]["ms_per_step"], 4),
+                "unshared_ms_per_step": u["ms_per_step"],
+                "kv_cache_bytes_shared": kv_bytes(wd), "kv_cache_bytes_unshared": kv_bytes(wi)}
+        if not args.no_extra:
+            result["decode_ragged_128k"] = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
 
     if not args.no_cpu:
-        log(f"[bench] oracle CPU baseline (first {args.cpu_seq} positions of one sequence)")
+        log(f"[bench] oracle CPU baseline ({args.cpu_seq} positions of one sequence)")
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seq)
 
     print(json.dumps(result), flush=True)
+
+
+def kv_bytes(w: ki.Workload) -> int:
+    """Resident KV-cache bytes of a decode workload (K and V^T slots of every producer)."""
+    return len(w.producers()) * 2 * w.batch * w.g * w.kv_capacity * w.d_h * 2
+
+
+def decode_entry(wd: ki.Workload, steps: int, warmup: int, alias_of=None):
+    log(f"[bench] decode {wd.name}")
+    dms, dprof, dfin, lens = bench_decode(wd, steps, warmup, alias_of=alias_of)
+    db = decode_bytes(wd, lens)
+    dtotal = sum(db.values())
+    n_a = dprof["dec_attn"][0]
+    ctx = int(np.sum(lens.astype(np.int64) + 1))
+    rl = roofline_entry("dec_attn", dprof, 2 * wd.g * wd.d_h * 2, ctx * wd.L * steps / n_a,
+                        PEAK_HBM_GBS, "GB/s", "hbm")
+    rl["per_unit"] = "bytes of K and V read for one cached position of one layer (g*d_h*2*2)"
+    out = {
+        "workload": wd.name, "batch": wd.batch, "context": [int(lens.min()), int(lens.max())],
+        "map": wd.tau, "tokens_per_s": round(wd.batch / (dms * 1e-3), 2),
+        "ms_per_step": round(dms, 4), "hbm_gbs": round(dtotal / (dms * 1e-3) / 1e9, 1),
+        "hbm_frac": round(dtotal / (dms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "bytes_per_step": dtotal, "kv_cache_bytes": kv_bytes(wd), "finite": dfin,
+        "roofline": rl,
+        "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in dprof.items()},
+    }
+    log(f"[bench] decode {dms:.3f} ms/step, {out['tokens_per_s']} tok/s, "
+        f"attention {rl['achieved']:.0f} GB/s")
+    return out
+
+
+def bench_70b(steps: int, warmup: int):
+    """The 70B-shaped stage: its map comes from the C++ planner (Algorithm 1) on the
+    stage-tail-heavy synthetic FLOPs of 80 layers over 8 stages, each stage's first layer
+    kept; the stage run on this GPU is the last one."""
+    from paper_2608_15943_amd import binding as kb
+    Lw = 80
+    t0 = time.perf_counter()
+    f0, f1 = kb.kvp_layer_flops(1, 8192, 8192, 64, 8, causal=True)
+    plan = kb.kvp_plan_fir([l // 10 for l in range(Lw)], [f0] * Lw, [f1] * Lw, 0.3 * 10 * f0, 0.05,
+                           admissible=[l % 10 != 0 for l in range(Lw)])
+    tau = kb.kvp_map_from_mask(plan["z"])
+    plan_us = (time.perf_counter() - t0) * 1e6
+    local = [t - 70 for t in tau[70:]]
+    w5 = ki.stage_70b_prefill(local)
+    log(f"[bench] prefill {w5.name} map {local} (planner {plan_us:.0f} us, FIR {plan['fir']:.4f})")
+    steps5 = max(3, steps // 2)
+    ms5, prof5, fin5 = bench_prefill(w5, steps5, max(1, warmup // 2))
+    fl5 = prefill_flops(w5, w5.batch, w5.seq)
+    dom5 = max(("qkv_gemm", "flash_attn", "oproj_gemm"), key=lambda k: prof5.get(k, (0, 0.0))[1])
+    rl = roofline_entry(dom5, prof5, fl5[dom5] / w5.L, w5.L * steps5 / prof5[dom5][0],
+                        PEAK_BF16_TFLOPS, "TFLOP/s", "mfma")
+    rl["per_unit"] = "algorithmic FLOPs of one layer (1 x 8192 tokens)"
+    out = {"workload": w5.name, "map": local, "planner": {"fir": plan["fir"],
+                                                          "n_converted": plan["n_converted"],
+                                                          "host_us": round(plan_us, 1)},
+           "tflops": round(sum(fl5.values()) / (ms5 * 1e-3) / 1e12, 2),
+           "ms_per_step": round(ms5, 4), "finite": fin5, "roofline": rl,
+           "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof5.items()},
+           "per_kernel_tflops": {k: round(fl5[k] * steps5 / prof5[k][1] / 1e9, 1)
+                                 for k in fl5 if k in prof5}}
+    log(f"[bench] 70B stage {ms5:.3f} ms/step, {out['tflops']} TFLOP/s")
+    return out
 
 
 if __name__ == "__main__":
