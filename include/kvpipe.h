@@ -43,8 +43,10 @@
  *   decode; cos/sin are evaluated in double precision.
  * - bf16 models compute every product in bf16 on matrix cores with fp32
  *   accumulation; Q, K, V, the softmax weights P and the attention output
- *   are rounded to bf16, and so is the residual stream.  fp32 models run
- *   every step in fp32 on the vector units (no reduced-precision modes).
+ *   are rounded to bf16.  Between layers the residual stream is carried in
+ *   fp32 (workspace), with a bf16 copy as the next projection's operand; the
+ *   caller's x and y are bf16.  fp32 models run every step in fp32 on the
+ *   vector units (no reduced-precision modes).
  */
 #ifndef KVPIPE_H
 #define KVPIPE_H
@@ -223,8 +225,8 @@ int kvp_set_kv_slot(kvp_ctx* ctx, int l, void* K, void* V);
 /*
  * kvp_workspace_size -- bytes of device scratch that a call with this phase,
  * batch B and length S (prefill; ignored for decode) needs.  The workspace
- * holds Q, the attention output, one residual buffer, the RoPE table
- * (prefill) and split-K partial results (decode).
+ * holds Q, the attention output, the fp32 residual stream and its bf16
+ * copy, the RoPE table (prefill) and split-K partial results (decode).
  * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY (B > max_batch, S > max_seq).
  */
 int kvp_workspace_size(const kvp_ctx* ctx, int phase, int B, int S, size_t* bytes);

@@ -39,6 +39,12 @@ hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint1
                               uint16_t* o, int B, int S, int a, int g, int cap, hipStream_t st);
 
 // ---- bf16 decode ------------------------------------------------------------
+// Largest decode grid (waves); the combine keeps one weight per wave of a pair in LDS.
+constexpr int kMaxDecodeSplits = 4096;
+
+// Partial-result slots the decode attention writes: one per (wave, pair) piece, at most
+// waves + B * g of them, r = a / g rows of decode_partial_floats() floats each.
+inline size_t decode_partial_floats() { return 132; }
 
 // out_f32 [M][N] = x @ w^T (M <= 64), or (out_f32 == nullptr) the residual update
 // y = x_res + x @ w^T with x_res in bf16 or (x_f32) fp32, y in bf16 and yf (optional) fp32.
@@ -46,12 +52,13 @@ hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int
                             float* out_f32, const void* x_res, bool x_f32, uint16_t* y, float* yf,
                             hipStream_t st);
 
-// Split-K attention of one new query per sequence over positions [0, len_b].
+// Attention of one new query per sequence over positions [0, len_b], on a grid of
+// `waves` single-wave workgroups that split the (sequence, KV head, tile) list evenly.
 hipError_t decode_attn_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                            const int32_t* lens, float* part, int B, int a, int g, int cap,
-                            int split, int nsplit, hipStream_t st);
-hipError_t decode_combine_bf16(const float* part, const int32_t* lens, uint16_t* o, int B, int a,
-                               int cap, int split, int nsplit, hipStream_t st);
+                            const int32_t* lens, float* part, int B, int a, int g, int cap, int waves,
+                            hipStream_t st);
+hipError_t decode_combine_bf16(const float* part, const int32_t* lens, uint16_t* o, int B, int a, int g,
+                               int cap, int waves, hipStream_t st);
 
 // ---- shared by both dtypes -------------------------------------------------
 

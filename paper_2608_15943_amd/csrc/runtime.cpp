@@ -44,9 +44,9 @@ struct Layer {
 };
 
 constexpr size_t kAlign = 256;
-constexpr int kMinSplit = 256;       // smallest decode split (positions per wave)
 constexpr int kDecodeMaxRows = 64;   // rows of the skinny decode GEMM
-constexpr int kTargetWaves = 4096;   // decode: split-K waves per layer to aim for
+// Decode attention: one single-wave workgroup per SIMD (4 per CU), all resident at once.
+constexpr int kSimdsPerCu = 4;
 
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -76,6 +76,7 @@ struct kvp_ctx {
     kvp_model_desc d;
     std::vector<int32_t> tau;
     std::vector<Layer> layers;
+    int decode_waves = 1024;          // decode attention grid: SIMDs of the device
     bool prof = false;
     std::vector<ProfRec> recs;        // launches timed since the last read
     std::vector<hipEvent_t> pool;     // idle events for reuse
@@ -117,8 +118,8 @@ Workspace layout(const kvp_ctx& c, int phase, int B, int S) {
     } else {
         w.proj = take(rows * nproj * sizeof(float));
         if (c.bf16()) {
-            const size_t nsplit = (c.d.kv_capacity + kMinSplit - 1) / kMinSplit;
-            w.part = take((size_t)B * c.d.a * nsplit * 132 * sizeof(float));
+            const size_t slots = (size_t)c.decode_waves + (size_t)B * c.d.g;
+            w.part = take(slots * (c.d.a / c.d.g) * kvp::decode_partial_floats() * sizeof(float));
         }
     }
     w.total = off;
@@ -276,16 +277,6 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
     });
 }
 
-int choose_split(const kvp_ctx* c, int B, int max_len, int* nsplit) {
-    const int total = max_len + 1;
-    const int pairs = B * c->d.g;
-    const int want = std::max(1, (kTargetWaves + pairs - 1) / pairs);
-    int split = (total + want - 1) / want;
-    split = std::max(kMinSplit, (split + 63) / 64 * 64);
-    *nsplit = (total + split - 1) / split;
-    return split;
-}
-
 int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
                      int max_len, char* ws, const Workspace& w, int B, hipStream_t st) {
     const int p = c->tau[l];
@@ -319,19 +310,17 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
          })))
         return rc;
     if (c->bf16()) {
-        int nsplit = 0;
-        const int split = choose_split(c, B, max_len, &nsplit);
         float* part = (float*)(ws + w.part);
         if ((rc = timed(c, KVP_K_DEC_ATTN, st, [&] {
                  return check_hip(kvp::decode_attn_bf16((const uint16_t*)q, (const uint16_t*)P.kc,
                                                         (const uint16_t*)P.vc, lens, part, B, c->d.a,
-                                                        c->d.g, c->d.kv_capacity, split, nsplit, st),
+                                                        c->d.g, c->d.kv_capacity, c->decode_waves, st),
                                   "decode attention");
              })))
             return rc;
         if ((rc = timed(c, KVP_K_DEC_COMBINE, st, [&] {
-                 return check_hip(kvp::decode_combine_bf16(part, lens, (uint16_t*)o, B, c->d.a,
-                                                           c->d.kv_capacity, split, nsplit, st),
+                 return check_hip(kvp::decode_combine_bf16(part, lens, (uint16_t*)o, B, c->d.a, c->d.g,
+                                                           c->d.kv_capacity, c->decode_waves, st),
                                   "decode combine");
              })))
             return rc;
@@ -408,6 +397,15 @@ extern "C" int kvp_create(const kvp_model_desc* desc, const int32_t* tau, kvp_ct
     c->d = d;
     c->tau = std::move(canon);
     c->layers.resize(d.L);
+    // Decode attention runs one wave per SIMD of the device current now; without a
+    // device (planning-only use) the MI355X's 256 CUs are assumed.
+    int dev = 0, cus = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cus > 0)
+        c->decode_waves = std::min(cus * kSimdsPerCu, kvp::kMaxDecodeSplits);
+    else
+        c->decode_waves = 256 * kSimdsPerCu;
+    (void)hipGetLastError();
     *out = c;
     return ok();
 }
