@@ -33,7 +33,8 @@ HIP_FLAGS = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}", "-I", INCLU
 HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math", "-I", INCLUDE,
               "-I", CSRC, "-Wall"]
 
-HIP_SOURCES = ["gemm_bf16.hip", "flash_prefill.hip", "decode_attn.hip", "small_kernels.hip"]
+HIP_SOURCES = ["gemm_bf16.hip", "flash_prefill.hip", "decode_attn.hip", "decode_gemm.hip",
+               "small_kernels.hip"]
 HIP_HOST_SOURCES = ["runtime.cpp"]   # host code that calls the HIP runtime
 HOST_SOURCES = ["planner.cpp"]       # pure host C++, no HIP
 

@@ -46,11 +46,22 @@ constexpr int kMaxDecodeSplits = 4096;
 // waves + B * g of them, r = a / g rows of decode_partial_floats() floats each.
 inline size_t decode_partial_floats() { return 132; }
 
-// out_f32 [M][N] = x @ w^T (M <= 64), or (out_f32 == nullptr) the residual update
-// y = x_res + x @ w^T with x_res in bf16 or (x_f32) fp32, y in bf16 and yf (optional) fp32.
-hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
-                            float* out_f32, const void* x_res, bool x_f32, uint16_t* y, float* yf,
+// Decode projections (M <= 64 rows, N % 128 == 0, K % 128 == 0): fp32 partial sums
+// part [decode_gemm_splits(K)][M][N] of x @ w^T, one plane per slice of K (512 wide
+// when 512 divides K, else 384, 256 or 128).
+int decode_gemm_splits(int K);
+hipError_t gemm_decode_bf16(const uint16_t* x, const WRows& w, int M, int N, int K, float* part,
                             hipStream_t st);
+// y = x_res + sum of the nsplit planes of part ([M][N] each); x_res bf16 or (x_f32) fp32,
+// y bf16 and yf (optional) fp32.  In place (y or yf == x_res) is allowed.
+hipError_t decode_resid_bf16(const float* part, int nsplit, int M, int N, const void* x_res, bool x_f32,
+                             uint16_t* y, float* yf, hipStream_t st);
+// Sum of the nsplit planes of part ([B][N], N = n_q (+ 2 n_kv for a producer)), RoPE at
+// position lens[b] (d_h = 128), then q [B][n_q] and, for a producer, the K row and V^T
+// column at position lens[b] of the slot.
+hipError_t decode_qkv_epilogue_bf16(const float* part, int nsplit, int B, int N, const int32_t* lens, int a,
+                                    int g, int cap, double base, bool producer, uint16_t* q, uint16_t* kc,
+                                    uint16_t* vc, hipStream_t st);
 
 // Attention of one new query per sequence over positions [0, len_b], on a grid of
 // `waves` single-wave workgroups that split the (sequence, KV head, tile) list evenly.
@@ -65,13 +76,13 @@ hipError_t decode_combine_bf16(const float* part, const int32_t* lens, uint16_t*
 // table[pos][i] = (cos, sin)(pos * base^(-2i/d)), evaluated in double.
 hipError_t rope_table(float2* table, int S, int d, double base, hipStream_t st);
 
-// RoPE + scatter of fp32 projections proj [rows][n_q + 2*n_kv]:
-// Q -> q [rows][n_q], K -> K slot, V -> V slot (transposed).  Row r is
-// sequence r / S at position r % S (lens == nullptr), or sequence r at
-// position lens[r].
-hipError_t rope_scatter(const float* proj, int rows, int S, const int32_t* lens, int a, int g,
-                        int d, int cap, double base, bool producer, bool bf16, void* q, void* kc,
-                        void* vc, hipStream_t st);
+// RoPE + scatter of fp32 projections proj [rows][n_q + 2*n_kv] (the sum of nsplit
+// planes split_stride floats apart): Q -> q [rows][n_q], K -> K slot, V -> V slot
+// (transposed).  Row r is sequence r / S at position r % S (lens == nullptr), or
+// sequence r at position lens[r].  d <= 128.
+hipError_t rope_scatter(const float* proj, int nsplit, size_t split_stride, int rows, int S,
+                        const int32_t* lens, int a, int g, int d, int cap, double base, bool producer,
+                        bool bf16, void* q, void* kc, void* vc, hipStream_t st);
 
 // ---- fp32 model path (vector ALU, full fp32) -------------------------------
 

@@ -116,7 +116,9 @@ Workspace layout(const kvp_ctx& c, int phase, int B, int S) {
         else
             w.proj = take(rows * nproj * sizeof(float));
     } else {
-        w.proj = take(rows * nproj * sizeof(float));
+        // bf16: one plane per 512-wide K slice of the projection GEMM (K = h for both GEMMs).
+        const size_t planes = c.bf16() ? (size_t)kvp::decode_gemm_splits(c.d.h) : 1;
+        w.proj = take(planes * rows * nproj * sizeof(float));
         if (c.bf16()) {
             const size_t slots = (size_t)c.decode_waves + (size_t)B * c.d.g;
             w.part = take(slots * (c.d.a / c.d.g) * kvp::decode_partial_floats() * sizeof(float));
@@ -256,7 +258,7 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
          })))
         return rc;
     if ((rc = timed(c, KVP_K_F32_ROPE, st, [&] {
-             return check_hip(kvp::rope_scatter(proj, M, S, nullptr, c->d.a, c->d.g, c->d.d_h,
+             return check_hip(kvp::rope_scatter(proj, 1, 0, M, S, nullptr, c->d.a, c->d.g, c->d.d_h,
                                                 c->d.kv_capacity, c->d.rope_base, producer, false, q,
                                                 producer ? P.kc : nullptr, producer ? P.vc : nullptr,
                                                 st),
@@ -292,21 +294,28 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
     void* q = ws + w.q;
     void* o = ws + w.o;
     int rc;
+    const int nsplit = c->bf16() ? kvp::decode_gemm_splits(h) : 1;
     if ((rc = timed(c, KVP_K_DEC_GEMM, st, [&] {
              return c->bf16()
-                        ? check_hip(kvp::gemm_skinny_bf16((const uint16_t*)io.a, wr, B, N, h, proj,
-                                                          nullptr, false, nullptr, nullptr, st),
+                        ? check_hip(kvp::gemm_decode_bf16((const uint16_t*)io.a, wr, B, N, h, proj, st),
                                     "decode projection GEMM")
                         : check_hip(kvp::gemm_f32((const float*)io.a, wr, B, N, h, proj, nullptr, st),
                                     "decode projection GEMM (fp32)");
          })))
         return rc;
     if ((rc = timed(c, KVP_K_DEC_ROPE, st, [&] {
-             return check_hip(kvp::rope_scatter(proj, B, 0, lens, c->d.a, c->d.g, c->d.d_h,
-                                                c->d.kv_capacity, c->d.rope_base, producer, c->bf16(),
-                                                q, producer ? P.kc : nullptr,
-                                                producer ? P.vc : nullptr, st),
-                              "decode RoPE + cache append");
+             return c->bf16()
+                        ? check_hip(kvp::decode_qkv_epilogue_bf16(
+                                        proj, nsplit, B, N, lens, c->d.a, c->d.g, c->d.kv_capacity,
+                                        c->d.rope_base, producer, (uint16_t*)q,
+                                        producer ? (uint16_t*)P.kc : nullptr,
+                                        producer ? (uint16_t*)P.vc : nullptr, st),
+                                    "decode RoPE + cache append")
+                        : check_hip(kvp::rope_scatter(proj, 1, 0, B, 0, lens, c->d.a, c->d.g, c->d.d_h,
+                                                      c->d.kv_capacity, c->d.rope_base, producer, false,
+                                                      q, producer ? P.kc : nullptr,
+                                                      producer ? P.vc : nullptr, st),
+                                    "decode RoPE + cache append");
          })))
         return rc;
     if (c->bf16()) {
@@ -325,9 +334,14 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
              })))
             return rc;
         return timed(c, KVP_K_DEC_OPROJ, st, [&] {
-            return check_hip(kvp::gemm_skinny_bf16((const uint16_t*)o, wo, B, h, nq, nullptr, io.res,
-                                                   io.res_f32, (uint16_t*)io.y, io.yf, st),
-                             "decode output projection");
+            const int ns = kvp::decode_gemm_splits(nq);
+            int r2 = check_hip(kvp::gemm_decode_bf16((const uint16_t*)o, wo, B, h, nq, proj, st),
+                               "decode output projection");
+            if (!r2)
+                r2 = check_hip(kvp::decode_resid_bf16(proj, ns, B, h, io.res, io.res_f32,
+                                                      (uint16_t*)io.y, io.yf, st),
+                               "decode residual");
+            return r2;
         });
     }
     if ((rc = timed(c, KVP_K_F32_ATTN, st, [&] {

@@ -3,8 +3,6 @@
 //   rope_scatter  -- RoPE on fp32 projections, then Q to its buffer and K, V
 //                    (transposed) into the producer's slot; used by decode
 //                    (position len_b of each sequence) and by fp32 models.
-//   gemm_skinny   -- decode projections, M = batch <= 64 rows, bf16 MFMA;
-//                    HBM-bound on the weights.
 //   gemm_f32, attn_f32 -- the full-precision path for fp32 models (vector
 //                    ALU, no reduced-precision matrix modes).
 #include <math.h>
@@ -51,9 +49,12 @@ template <>
 __device__ __forceinline__ void put<uint16_t>(uint16_t* p, size_t i, float v) { p[i] = f2bf(v); }
 
 template <typename T>
-__global__ void rope_scatter_kernel(const float* __restrict__ proj, int S,
-                                    const int32_t* __restrict__ lens, int a, int g, int d, int cap,
-                                    double base, int producer, T* q, T* kc, T* vc) {
+__global__ __launch_bounds__(256) void rope_scatter_kernel(const float* __restrict__ proj, int nsplit,
+                                                           size_t split_stride, int S,
+                                                           const int32_t* __restrict__ lens, int a,
+                                                           int g, int d, int cap, double base,
+                                                           int producer, T* q, T* kc, T* vc) {
+    __shared__ float2 cs[64];                 // (cos, sin) of this row's position, d / 2 <= 64
     const int r = blockIdx.x;
     int b, pos;
     if (lens) {
@@ -64,15 +65,26 @@ __global__ void rope_scatter_kernel(const float* __restrict__ proj, int S,
         pos = r - b * S;
     }
     const int half = d / 2, nq = a * d, nkv = g * d;
-    const float* pr = proj + (size_t)r * (nq + (producer ? 2 * nkv : 0));
-    const int heads = a + (producer ? g : 0);
-    for (int j = threadIdx.x; j < heads * half; j += blockDim.x) {
-        const int h = j / half, i = j - h * half;
+    const int ncols = nq + (producer ? 2 * nkv : 0);
+    const float* pr = proj + (size_t)r * ncols;
+    // Sum of the K slices of the projection (one slice unless the GEMM split K).
+    auto val = [&](int c) {
+        float v = pr[c];
+        for (int s = 1; s < nsplit; ++s) v += pr[(size_t)s * split_stride + c];
+        return v;
+    };
+    for (int i = threadIdx.x; i < half; i += blockDim.x) {
         const double theta = pow(base, -2.0 * i / d);
         double sd, cd;
         sincos((double)pos * theta, &sd, &cd);
-        const float c = (float)cd, s = (float)sd;
-        const float x1 = pr[h * d + i], x2 = pr[h * d + i + half];
+        cs[i] = make_float2((float)cd, (float)sd);
+    }
+    __syncthreads();
+    const int heads = a + (producer ? g : 0);
+    for (int j = threadIdx.x; j < heads * half; j += blockDim.x) {
+        const int h = j / half, i = j - h * half;
+        const float c = cs[i].x, s = cs[i].y;
+        const float x1 = val(h * d + i), x2 = val(h * d + i + half);
         const float o1 = x1 * c - x2 * s, o2 = x2 * c + x1 * s;
         if (h < a) {
             put(q, (size_t)r * nq + h * d + i, o1);
@@ -86,74 +98,7 @@ __global__ void rope_scatter_kernel(const float* __restrict__ proj, int S,
     if (producer) {
         for (int j = threadIdx.x; j < nkv; j += blockDim.x) {
             const int h = j / d, c = j - h * d;
-            put(vc, (((size_t)b * g + h) * d + c) * cap + pos, pr[nq + nkv + j]);
-        }
-    }
-}
-
-// ---------------------------------------------------------------------------
-// Skinny bf16 GEMM for decode: a workgroup owns 16 output columns; its four
-// waves split K and meet in LDS at the end.
-// ---------------------------------------------------------------------------
-
-constexpr int SK_THREADS = 256;
-
-__global__ __launch_bounds__(SK_THREADS) void gemm_skinny_kernel(
-    const uint16_t* __restrict__ X, WRows W, int M, int N, int K, float* __restrict__ out,
-    const void* xres, int xres_f32, uint16_t* __restrict__ y, float* yf) {
-    __shared__ f32x4 red[4][4][64];   // [wave][m block][lane]
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int col = lane & 15, grp = lane >> 4;
-    const int n = blockIdx.x * 16 + col;
-    const uint16_t* wr = (const uint16_t*)w_row_any(W, min(n, N - 1), K, 2);
-    const int nmb = (M + 15) / 16;
-
-    const uint16_t* xr[4];
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) xr[mb] = X + (size_t)min(16 * mb + col, M - 1) * K;
-
-    f32x4 acc[4];
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) acc[mb] = f32x4{};
-
-    // Wave w takes the 128-wide K chunks w, w + 4, w + 8, ... (K % 128 == 0).
-    for (int k = wave * 128; k < K; k += 512) {
-        u32x4 wf[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) wf[j] = *(const u32x4*)(wr + k + 32 * j + 8 * grp);
-#pragma unroll
-        for (int mb = 0; mb < 4; ++mb) {
-            if (mb < nmb) {
-#pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const u32x4 xf = *(const u32x4*)(xr[mb] + k + 32 * j + 8 * grp);
-                    acc[mb] = mfma16x16x32(as_bf16x8(xf), as_bf16x8(wf[j]), acc[mb]);
-                }
-            }
-        }
-    }
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) red[wave][mb][lane] = acc[mb];
-    __syncthreads();
-    if (wave != 0) return;
-#pragma unroll
-    for (int mb = 0; mb < 4; ++mb) {
-        if (mb >= nmb) break;
-        const f32x4 v = red[0][mb][lane] + red[1][mb][lane] + red[2][mb][lane] + red[3][mb][lane];
-#pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int m = 16 * mb + 4 * grp + i;
-            if (m < M && n < N) {
-                const size_t off = (size_t)m * N + n;
-                if (out) {
-                    out[off] = v[i];
-                } else {
-                    const float r = (xres_f32 ? ((const float*)xres)[off]
-                                              : bf2f(((const uint16_t*)xres)[off])) + v[i];
-                    y[off] = f2bf(r);
-                    if (yf) yf[off] = r;
-                }
-            }
+            put(vc, (((size_t)b * g + h) * d + c) * cap + pos, val(nq + nkv + j));
         }
     }
 }
@@ -259,25 +204,19 @@ hipError_t rope_table(float2* table, int S, int d, double base, hipStream_t st) 
     return hipGetLastError();
 }
 
-hipError_t rope_scatter(const float* proj, int rows, int S, const int32_t* lens, int a, int g,
-                        int d, int cap, double base, bool producer, bool bf16, void* q, void* kc,
-                        void* vc, hipStream_t st) {
+hipError_t rope_scatter(const float* proj, int nsplit, size_t split_stride, int rows, int S,
+                        const int32_t* lens, int a, int g, int d, int cap, double base, bool producer,
+                        bool bf16, void* q, void* kc, void* vc, hipStream_t st) {
     if (rows <= 0) return hipSuccess;
+    if (d > 128 || nsplit < 1) return hipErrorInvalidValue;
     if (bf16)
-        hipLaunchKernelGGL(rope_scatter_kernel<uint16_t>, dim3(rows), dim3(256), 0, st, proj, S, lens,
-                           a, g, d, cap, base, producer ? 1 : 0, (uint16_t*)q, (uint16_t*)kc,
-                           (uint16_t*)vc);
+        hipLaunchKernelGGL(rope_scatter_kernel<uint16_t>, dim3(rows), dim3(256), 0, st, proj, nsplit,
+                           split_stride, S, lens, a, g, d, cap, base, producer ? 1 : 0, (uint16_t*)q,
+                           (uint16_t*)kc, (uint16_t*)vc);
     else
-        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(rows), dim3(256), 0, st, proj, S, lens, a,
-                           g, d, cap, base, producer ? 1 : 0, (float*)q, (float*)kc, (float*)vc);
-    return hipGetLastError();
-}
-
-hipError_t gemm_skinny_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
-                            float* out_f32, const void* x_res, bool x_f32, uint16_t* y, float* yf,
-                            hipStream_t st) {
-    hipLaunchKernelGGL(gemm_skinny_kernel, dim3((N + 15) / 16), dim3(SK_THREADS), 0, st, x, w, M, N, K,
-                       out_f32, x_res, x_f32 ? 1 : 0, y, yf);
+        hipLaunchKernelGGL(rope_scatter_kernel<float>, dim3(rows), dim3(256), 0, st, proj, nsplit,
+                           split_stride, S, lens, a, g, d, cap, base, producer ? 1 : 0, (float*)q,
+                           (float*)kc, (float*)vc);
     return hipGetLastError();
 }
 
