@@ -283,6 +283,8 @@ def main():
     ap.add_argument("--cpu-seq", type=int, default=4096)
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the 70B-shaped prefill and the ragged 128K decode lines")
+    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k"],
+                    help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
     args = ap.parse_args()
@@ -300,6 +302,21 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     kb.lib()   # fail loudly if the HIP library is missing
+    if args.only:
+        steps_d, warm_d = max(3, args.steps // 2), max(1, args.warmup // 2)
+        if args.only == "prefill_70b":
+            out = bench_70b(args.steps, args.warmup)
+        elif args.only == "decode":
+            out = decode_entry(ki.decode_32k(), steps_d, warm_d)
+        elif args.only == "decode_128k":
+            out = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
+        else:
+            w = ki.stage_share_prefill()
+            ms, prof, finite = bench_prefill(w, args.steps, args.warmup)
+            out = {"workload": w.name, "ms_per_step": round(ms, 4), "finite": finite,
+                   "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof.items()}}
+        print(json.dumps({"only": args.only, **out}), flush=True)
+        return
 
     w = ki.stage_share_prefill()
     log(f"[bench] prefill {w.name} steps={args.steps} warmup={args.warmup}")
