@@ -237,27 +237,27 @@ def calibrate_copy():
     print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 5}))
 
 
-def roofline_entry(kernel, prof, per_unit, units_per_launch, peak, unit, bound):
+def roofline_entry(kernel, prof, per_unit, units_per_launch, peak, unit, bound, workload):
     """Algorithmic work per launch (per-unit figure x units one launch processes) over the
     kernel's average launch time, measured with HIP events on the launch stream."""
     n, t = prof[kernel]
     per_launch = per_unit * units_per_launch
     achieved = per_launch / (t / n * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
     return {"bound": bound, "kernel": kernel, "achieved": round(achieved, 2), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel),
+            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel, workload),
             "work_per_launch": per_launch, "avg_launch_ms": round(t / n, 5)}
 
 
-def traffic_for(kernel):
+def traffic_for(kernel, workload):
     """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE counter runs (scaled by
-    the factor a plain copy of known size gives), or None once the kernel's sources differ
-    from the ones the counters were taken on."""
+    the factor a plain copy of known size gives) of this kernel on this workload, or None if
+    there is none or the kernel's sources differ from the ones the counters were taken on."""
     import hashlib
     path = os.path.join(ROOT, "profiles", "traffic.json")
     if not os.path.exists(path):
         return None
     with open(path) as f:
-        ent = json.load(f).get(kernel)
+        ent = json.load(f).get(f"{kernel}@{workload}")
     if not ent:
         return None
     h = hashlib.sha1()
@@ -328,7 +328,7 @@ def main():
     dom = max(("qkv_gemm", "flash_attn", "oproj_gemm"), key=lambda k: prof.get(k, (0, 0.0))[1])
     n_l = prof[dom][0]
     roofline = roofline_entry(dom, prof, flops[dom] / w.L, w.L * args.steps / n_l,
-                              PEAK_BF16_TFLOPS, "TFLOP/s", "mfma")
+                              PEAK_BF16_TFLOPS, "TFLOP/s", "mfma", w.name)
     roofline["per_unit"] = "algorithmic FLOPs of one layer of the stack (batch 4 x 4096 tokens)"
     log(f"[bench] prefill {ms:.3f} ms/step, {value:.1f} TFLOP/s; kernels {kernels}")
 
@@ -398,7 +398,7 @@ def decode_entry(wd: ki.Workload, steps: int, warmup: int, alias_of=None):
     n_a = dprof["dec_attn"][0]
     ctx = int(np.sum(lens.astype(np.int64) + 1))
     rl = roofline_entry("dec_attn", dprof, 2 * wd.g * wd.d_h * 2, ctx * wd.L * steps / n_a,
-                        PEAK_HBM_GBS, "GB/s", "hbm")
+                        PEAK_HBM_GBS, "GB/s", "hbm", wd.name)
     rl["per_unit"] = "bytes of K and V read for one cached position of one layer (g*d_h*2*2)"
     out = {
         "workload": wd.name, "batch": wd.batch, "context": [int(lens.min()), int(lens.max())],
@@ -434,7 +434,7 @@ def bench_70b(steps: int, warmup: int):
     fl5 = prefill_flops(w5, w5.batch, w5.seq)
     dom5 = max(("qkv_gemm", "flash_attn", "oproj_gemm"), key=lambda k: prof5.get(k, (0, 0.0))[1])
     rl = roofline_entry(dom5, prof5, fl5[dom5] / w5.L, w5.L * steps5 / prof5[dom5][0],
-                        PEAK_BF16_TFLOPS, "TFLOP/s", "mfma")
+                        PEAK_BF16_TFLOPS, "TFLOP/s", "mfma", w5.name)
     rl["per_unit"] = "algorithmic FLOPs of one layer (1 x 8192 tokens)"
     out = {"workload": w5.name, "map": local, "planner": {"fir": plan["fir"],
                                                           "n_converted": plan["n_converted"],
