@@ -84,6 +84,13 @@ def test_bf16_stack(h, a, g, tau, B, S):
     _prefill_case(w, B, S, cap)
 
 
+def test_bf16_stack_capacity_equals_length():
+    """kv_capacity == S with S % 128 == 64: the last 128-position key tile of the
+    prefill attention runs past the slot and must not read or use anything there."""
+    w = small_workload("bf16-h512-a4-g2-capS", 3, 512, 4, 2, [0, 0, 2])
+    _prefill_case(w, 2, 320, 320)
+
+
 def test_bf16_layer_forward_producer_then_consumer():
     """kvp_layer_forward on seeded inputs: attention output and residual per layer."""
     w = small_workload("bf16-layers", 2, 512, 4, 2, [0, 0])
