@@ -165,8 +165,7 @@ __global__ __launch_bounds__(64, 1) void decode_attn_kernel(
                 }
                 mx = fmaxf(mx, sc[tb][i]);
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        mx = pair32_max(pair16_max(mx));
         const float mt = mx * scale_log2;
         if (__any(mt > m_run + kLazy)) {
             const float m_new = fmaxf(m_run, mt);
@@ -216,8 +215,7 @@ __global__ __launch_bounds__(64, 1) void decode_attn_kernel(
 
         if (pair_ends) {
             // ---- partial result of this wave's piece of pair (b, kvh) -----------------
-            float lt = l_run + __shfl_xor(l_run, 16);
-            lt += __shfl_xor(lt, 32);
+            const float lt = pair32_sum(pair16_sum(l_run));
             if (col < r) {
                 float* pr = part + (((size_t)w + (size_t)b * g + kvh) * r + col) * PSTRIDE;
                 // O^T block db: lane holds dims 16 db + 4 grp + 0..3 of head col.

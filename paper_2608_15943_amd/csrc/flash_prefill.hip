@@ -171,7 +171,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
                 for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[mb][i]);
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            mx = pair32_max(mx);
             const float mt = mx * scale_log2;                  // tile max, log2 domain
             if (__any(mt > m_run + kLazy)) {
                 const float m_new = fmaxf(m_run, mt);
@@ -226,7 +226,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     // ---- normalise and store O[b, q, head, :] -------------------------------------
     // Lanes q and q ^ 32 hold the same query, so both take this branch or neither.
     if (q_lane < S) {
-        const float l_tot = l_run + __shfl_xor(l_run, 32);
+        const float l_tot = pair32_sum(l_run);
         const float inv = 1.0f / l_tot;
         uint16_t* orow = O + ((size_t)b * S + q_lane) * ldq + head * D;
 #pragma unroll
