@@ -201,13 +201,27 @@ def bench_decode(w: ki.Workload, steps: int, warmup: int, alias_of=None):
 # CPU baseline: the oracle on a bounded sample of the prefill workload
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(w: ki.Workload, s_sample: int):
-    from oracle import attention as oat
+def host_info():
+    """Host cores, BLAS threads and CPU model, reported with every oracle figure."""
     try:
         from threadpoolctl import threadpool_info
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:
         threads = os.cpu_count() or 1
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    return int(threads), {"os_cpu_count": os.cpu_count(), "blas_threads": int(threads), "cpu_model": model}
+
+
+def oracle_weights(w: ki.Workload):
+    from oracle import attention as oat
     ws = []
     for l in range(w.L):
         prod = w.tau[l] == l
@@ -215,17 +229,47 @@ def cpu_baseline(w: ki.Workload, s_sample: int):
                                    ki.weight(w, ki.KIND_WK, l) if prod else None,
                                    ki.weight(w, ki.KIND_WV, l) if prod else None,
                                    ki.weight(w, ki.KIND_WO, l)))
+    return ws
+
+
+def cpu_baseline(w: ki.Workload, s_sample: int):
+    from oracle import attention as oat
+    threads, host = host_info()
+    ws = oracle_weights(w)
     x = ki.prefill_x(w, [0], np.arange(s_sample))[0]
     t0 = time.perf_counter()
     oat.stack_prefill(x, ws, w.tau, w.a, w.g, w.d_h, w.rope_base)
     dt = time.perf_counter() - t0
     flops = sum(prefill_flops(w, 1, s_sample).values())
-    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
             "kind": "oracle",
             "sample": (f"sequence 0 of {w.batch}, " +
                        (f"all {s_sample} positions" if s_sample == w.seq else
                         f"first {s_sample} positions (causal prefix, exact)") +
-                       f", all {w.L} layers, fp64 NumPy with host BLAS; {dt:.1f} s")}
+                       f", all {w.L} layers, fp64 NumPy with host BLAS; {dt:.1f} s"),
+            "host": host}
+
+
+def cpu_baseline_decode(wd: ki.Workload, lens, sample: int = 0):
+    """The oracle's decode step for one sequence of the batch through all layers (rows of a
+    batch never interact, so one sequence is an exact sample); the time to regenerate its
+    cache from the seeded generator is excluded and reported separately."""
+    from oracle import attention as oat
+    threads, host = host_info()
+    L = int(lens[sample])
+    t0 = time.perf_counter()
+    caches = {p: (ki.cache_contents(wd, ki.KIND_KCACHE, p, sample, L),
+                  ki.cache_contents(wd, ki.KIND_VCACHE, p, sample, L)) for p in wd.producers()}
+    ws = oracle_weights(wd)
+    x = ki.decode_x(wd, [sample])[0]
+    t1 = time.perf_counter()
+    oat.decode_step(x, L, ws, wd.tau, caches, wd.a, wd.g, wd.d_h, wd.rope_base)
+    dt = time.perf_counter() - t1
+    return {"value": round(1.0 / dt, 4), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": (f"sequence {sample} of {wd.batch} ({L} cached positions), all {wd.L} layers, "
+                       f"fp64 NumPy with host BLAS; {dt:.2f} s (cache regeneration "
+                       f"{t1 - t0:.1f} s, not counted)"),
+            "host": host}
 
 
 def calibrate_copy():
@@ -369,6 +413,9 @@ def main():
         steps_d, warm_d = max(3, args.steps // 2), max(1, args.warmup // 2)
         wd = ki.decode_32k()
         result["decode"] = decode_entry(wd, steps_d, warm_d)
+        if not args.no_cpu:
+            log("[bench] oracle CPU baseline (decode, one sequence)")
+            result["decode"]["cpu_baseline"] = cpu_baseline_decode(wd, wd.lengths())
         if not args.no_unshared:
             # Identity map: every layer owns a cache.  All 32 caches (275 GB) do not fit
             # beside the rest, so former consumers reuse their former producer's memory;
