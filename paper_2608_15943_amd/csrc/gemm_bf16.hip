@@ -301,15 +301,17 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
         a_src[j] = A + (size_t)min(m0 + row, M - 1) * K + 8 * c;
         w_src[j] = w_row(W, min(n0 + row, N - 1), K) + 8 * c;
     }
+    // Row group j (8 rows of A and of W) of tile kt into stage stg.
+    auto issue_part = [&](int kt, int stg, int j) {
+        const int r0 = 64 * wave + 8 * j;
+        __builtin_amdgcn_global_load_lds((gvoid_t*)(a_src[j] + kt * BK), (lvoid_t*)&lds[stg][0][r0 * 8], 16,
+                                         0, 0);
+        __builtin_amdgcn_global_load_lds((gvoid_t*)(w_src[j] + kt * BK), (lvoid_t*)&lds[stg][1][r0 * 8], 16,
+                                         0, 0);
+    };
     auto issue = [&](int kt, int stg) {
 #pragma unroll
-        for (int j = 0; j < 8; ++j) {
-            const int r0 = 64 * wave + 8 * j;
-            __builtin_amdgcn_global_load_lds((gvoid_t*)(a_src[j] + kt * BK), (lvoid_t*)&lds[stg][0][r0 * 8],
-                                             16, 0, 0);
-            __builtin_amdgcn_global_load_lds((gvoid_t*)(w_src[j] + kt * BK), (lvoid_t*)&lds[stg][1][r0 * 8],
-                                             16, 0, 0);
-        }
+        for (int j = 0; j < 8; ++j) issue_part(kt, stg, j);
     };
 
     f32x16 acc[4][4];
@@ -347,12 +349,19 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
     for (int kt = 0; kt < nk; ++kt) {
         const int cur = kt & 1;
         const bool more = kt + 1 < nk;
-        // The other buffer was last read before the barrier that ended step kt - 1.
-        if (more) issue(kt + 1, cur ^ 1);
         // Four 16-wide k steps; the fragments of step ks + 1 are read from LDS while the
         // 16 MFMAs of step ks run (one ds_read slotted after each of the first 8 MFMAs).
+        // Tile kt + 1 goes into the other buffer (last read before the barrier that ended
+        // step kt - 1) in two halves, with the first two k steps: issued in one burst its
+        // LDS writes collide with the fragment reads; spread over all four steps the last
+        // loads land too close to the end-of-tile wait (measured: 4 % / 5 % faster GEMMs
+        // than the burst at K = 2048 / 8192).
 #pragma unroll
         for (int ks = 0; ks < 4; ++ks) {
+            if (more && ks < 2) {
+#pragma unroll
+                for (int j = 0; j < 4; ++j) issue_part(kt + 1, cur ^ 1, 4 * ks + j);
+            }
             if (ks < 3) load_frags(cur, ks + 1, ga, gb);
 #pragma unroll
             for (int mb = 0; mb < 4; ++mb)
