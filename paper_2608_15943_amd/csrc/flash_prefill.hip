@@ -136,7 +136,8 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
 
     for (int t = 0; t < ntiles; ++t) {
         const int stg = t & 1;
-        if (t + 1 < ntiles) issue_tile(t + 1, stg ^ 1);
+        const bool more = t + 1 < ntiles;
+        bool issued = false;
 
         const int t0 = t * BKV;
         if (t0 <= q0w + 31 && q0w < S) {          // some key of the tile is visible to this wave
@@ -154,6 +155,10 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 s[2] = mfma32x32x16(k2, qf[ks], s[2]);
                 s[3] = mfma32x32x16(k3, qf[ks], s[3]);
             }
+            // The next tile goes into the other buffer (read last before the previous barrier)
+            // after the K fragment reads of this one, not in the same burst (1-2 % faster).
+            if (more) issue_tile(t + 1, stg ^ 1);
+            issued = true;
             // Register i of block mb holds position t0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
             const bool diag = (t0 + BKV - 1 > q0w) || (t0 + BKV > S);
             if (diag) {
@@ -211,6 +216,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 }
             }
         }
+        if (more && !issued) issue_tile(t + 1, stg ^ 1);   // this wave saw no key of tile t
         // One barrier: tile t + 1 has landed in LDS (every wave waited for its own loads)
         // and every wave is done reading tile t, whose buffer is refilled next.
         if (t + 1 < ntiles) {
