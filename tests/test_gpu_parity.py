@@ -77,6 +77,8 @@ def test_fp32_ragged_two_sequences():
     (1024, 8, 1, [0, 0], 1, 130),            # r=8, S just past a query tile
     (256, 2, 1, [0, 1], 3, 1),               # S = 1
     (256, 2, 1, [0, 1], 5, 3),               # S < 4: one 4-row group spans sequences
+    (512, 4, 2, [0, 0, 2], 4, 300),          # B*g = 8: whole KV-head groups per XCD
+    (512, 4, 4, [0, 1], 4, 520),             # B*g = 16, r=1, three query tiles
 ])
 def test_bf16_stack(h, a, g, tau, B, S):
     w = small_workload(f"bf16-h{h}-a{a}-g{g}", len(tau), h, a, g, tau)
