@@ -13,8 +13,10 @@ A step is one pass of the whole path over one batch of synthetic input:
   stack (batch 64, 32768-token caches, odd layers share) in tokens/s and
   algorithmic HBM GB/s.
 The JSON line also carries the roofline of the dominant kernel (timed with HIP
-events on its own stream), the oracle's rate on the host cores, and the
-shared-vs-unshared (identity map) ratio.
+events on its own stream) against the datasheet peak and against the peak this
+device measurably delivers (a bf16 matrix-core loop and a streaming read, run
+first), the oracle's rate on the host cores, and the shared-vs-unshared
+(identity map) ratio.
 """
 from __future__ import annotations
 
@@ -286,15 +288,61 @@ def calibrate_copy():
     print(json.dumps({"calibration": "device copy", "bytes_read": n, "bytes_written": n, "launches": 5}))
 
 
+ACHIEVABLE = {}
+
+
+def achievable_peaks():
+    """What this device delivers, measured with the library's calibration kernels
+    (include/kvp_calib.h): a bf16 matrix-core loop with operands that change every
+    instruction, and a streaming read of a 4 GiB buffer (16x the last-level cache).  Best of
+    five timed launches each, HIP events on the launch stream."""
+    import torch
+    from paper_2608_15943_amd import binding as kb
+    st = torch.cuda.current_stream()
+    sink = torch.zeros(64, dtype=torch.uint8, device="cuda")
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def best(launch):
+        launch()
+        t = []
+        for _ in range(5):
+            e0.record(st)
+            launch()
+            e1.record(st)
+            e1.synchronize()
+            t.append(e0.elapsed_time(e1))
+        return min(t)
+    iters = 20000
+    flops = kb.kvp_calib_mfma_bf16(iters, sink.data_ptr(), st.cuda_stream)
+    ms = best(lambda: kb.kvp_calib_mfma_bf16(iters, sink.data_ptr(), st.cuda_stream))
+    n = 4 << 30
+    buf = torch.empty(n // 8, dtype=torch.int64, device="cuda").random_()
+    ms_r = best(lambda: kb.kvp_calib_stream_read(buf.data_ptr(), n, sink.data_ptr(), st.cuda_stream))
+    del buf
+    torch.cuda.empty_cache()
+    ACHIEVABLE.update({
+        "mfma_bf16_tflops": round(flops / (ms * 1e-3) / 1e12, 1),
+        "hbm_read_gbs": round(n / (ms_r * 1e-3) / 1e9, 1),
+        "method": "kvp_calib_mfma_bf16 (8 waves per CU, v_mfma_f32_32x32x16_bf16 on random bf16 "
+                  "operands, 20000 x 16 per wave) and kvp_calib_stream_read (4 GiB), best of 5"})
+    return dict(ACHIEVABLE)
+
+
 def roofline_entry(kernel, prof, per_unit, units_per_launch, peak, unit, bound, workload):
     """Algorithmic work per launch (per-unit figure x units one launch processes) over the
     kernel's average launch time, measured with HIP events on the launch stream."""
     n, t = prof[kernel]
     per_launch = per_unit * units_per_launch
     achieved = per_launch / (t / n * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
-    return {"bound": bound, "kernel": kernel, "achieved": round(achieved, 2), "peak": peak,
-            "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel, workload),
-            "work_per_launch": per_launch, "avg_launch_ms": round(t / n, 5)}
+    ent = {"bound": bound, "kernel": kernel, "achieved": round(achieved, 2), "peak": peak,
+           "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel, workload),
+           "work_per_launch": per_launch, "avg_launch_ms": round(t / n, 5)}
+    # The same figure against what this device measurably delivers (achievable_peaks).
+    ach = ACHIEVABLE.get("mfma_bf16_tflops" if unit == "TFLOP/s" else "hbm_read_gbs")
+    if ach:
+        ent["peak_achievable"] = ach
+        ent["frac_achievable"] = round(achieved / ach, 4)
+    return ent
 
 
 def traffic_for(kernel, workload):
@@ -332,7 +380,9 @@ def main():
     ap.add_argument("--cpu-seq", type=int, default=4096)
     ap.add_argument("--no-extra", action="store_true",
                     help="skip the 70B-shaped prefill and the ragged 128K decode lines")
-    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k"],
+    ap.add_argument("--no-calib", action="store_true",
+                    help="skip the achievable-peak calibration (no frac_achievable figures)")
+    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
@@ -351,6 +401,11 @@ def main():
         print("bench.py needs a GPU", file=sys.stderr)
         sys.exit(1)
     kb.lib()   # fail loudly if the HIP library is missing
+    if args.only == "calib":
+        print(json.dumps({"only": "calib", **achievable_peaks()}), flush=True)
+        return
+    if not args.no_calib and not args.only:
+        log(f"[bench] achievable peaks {achievable_peaks()}")
     if args.only:
         steps_d, warm_d = max(3, args.steps // 2), max(1, args.warmup // 2)
         if args.only == "prefill_70b":
@@ -391,6 +446,7 @@ def main():
                    "kv_heads": w.g, "head_dim": w.d_h, "batch": w.batch, "seq_len": w.seq,
                    "causal": True, "map": w.tau, "parallelism": "none (1 GPU)"},
         "roofline": roofline,
+        "achievable": dict(ACHIEVABLE) or None,
         "kernels": kernels,
         "per_kernel_tflops": {k: round(flops[k] * args.steps / prof[k][1] / 1e9, 1)
                               for k in flops if k in prof},

@@ -37,6 +37,8 @@ EXPORTS = [
     "kvp_create", "kvp_destroy", "kvp_set_layer", "kvp_set_kv_slot", "kvp_workspace_size",
     "kvp_prefill", "kvp_layer_forward", "kvp_decode_step", "kvp_get_map", "kvp_status_string",
     "kvp_last_error", "kvp_profile_enable", "kvp_profile_read",
+    # include/kvp_calib.h: achievable-peak calibration (measurement support)
+    "kvp_calib_mfma_bf16", "kvp_calib_stream_read",
 ]
 
 KERNEL_KINDS = ["rope_table", "qkv_gemm", "flash_attn", "oproj_gemm", "dec_gemm", "dec_rope",
@@ -104,6 +106,8 @@ def lib() -> C.CDLL:
         "kvp_last_error": ([], C.c_char_p),
         "kvp_profile_enable": ([vp, i32], i32),
         "kvp_profile_read": ([vp, C.POINTER(dbl), C.POINTER(i64)], i32),
+        "kvp_calib_mfma_bf16": ([i32, vp, C.POINTER(dbl), vp], i32),
+        "kvp_calib_stream_read": ([vp, C.c_size_t, vp, vp], i32),
     }
     for name, (args, res) in sig.items():
         fn = getattr(L, name)
@@ -243,3 +247,19 @@ class Model:
         tau = (C.c_int32 * self.L)()
         _check(lib().kvp_get_map(self.ctx, tau), "kvp_get_map")
         return list(tau)
+
+
+# ---- achievable-peak calibration (include/kvp_calib.h) ---------------------------------
+
+def kvp_calib_mfma_bf16(iters: int, sink: int, stream: int = 0) -> float:
+    """Launch the bf16 matrix-core loop; returns the launch's floating-point operations."""
+    flops = C.c_double()
+    _check(lib().kvp_calib_mfma_bf16(int(iters), C.c_void_p(sink), C.byref(flops), C.c_void_p(stream)),
+           "kvp_calib_mfma_bf16")
+    return flops.value
+
+
+def kvp_calib_stream_read(src: int, nbytes: int, sink: int, stream: int = 0) -> None:
+    """Launch the streaming read of nbytes at device address src."""
+    _check(lib().kvp_calib_stream_read(C.c_void_p(src), C.c_size_t(nbytes), C.c_void_p(sink),
+                                       C.c_void_p(stream)), "kvp_calib_stream_read")

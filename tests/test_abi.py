@@ -200,3 +200,17 @@ def test_workspace_and_call_checks():
     with pytest.raises(kb.KvpError) as e:            # B > max_batch
         m.kvp_decode_step(fake, fake * 8, 10, fake * 2, 3, fake * 4, nd)
     assert e.value.code == kb.KVP_E_CAPACITY
+
+
+def test_calibration_entry_points_reject_bad_arguments():
+    """include/kvp_calib.h: argument checks happen on the host, before any launch."""
+    L = kb.lib()
+    import ctypes as C
+    f = C.c_double()
+    assert L.kvp_calib_mfma_bf16(0, C.c_void_p(16), C.byref(f), None) == kb.KVP_E_INVALID_ARG
+    assert L.kvp_calib_mfma_bf16(3, C.c_void_p(16), C.byref(f), None) == kb.KVP_E_INVALID_ARG
+    assert L.kvp_calib_mfma_bf16(2, None, C.byref(f), None) == kb.KVP_E_INVALID_ARG
+    assert L.kvp_calib_stream_read(None, 65536, C.c_void_p(16), None) == kb.KVP_E_INVALID_ARG
+    assert L.kvp_calib_stream_read(C.c_void_p(256), 1000, C.c_void_p(16), None) == kb.KVP_E_INVALID_ARG
+    assert L.kvp_calib_stream_read(C.c_void_p(258), 65536, C.c_void_p(16), None) == kb.KVP_E_INVALID_ARG
+    assert "kvp_calib_stream_read" in L.kvp_last_error().decode()
