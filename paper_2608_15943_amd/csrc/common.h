@@ -22,8 +22,6 @@ typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 constexpr int kWave = 64;
 constexpr int kNumXcd = 8;  // MI355X: 8 XCDs, workgroups are dealt to them round-robin
 
-__device__ __forceinline__ float bf2f(bf16_t v) { return __uint_as_float((uint32_t)v << 16); }
-
 // Round to nearest even (the hardware conversion on gfx950).
 __device__ __forceinline__ bf16_t f2bf(float f) {
     __bf16 b = (__bf16)f;
