@@ -61,6 +61,10 @@ __device__ __forceinline__ u32x4 ld_f32(const char* st, int m, int c) {
 // transposed ([n][m], 8-byte unit u of row n at position u ^ (n & 31)).
 struct QkvEpi {
     static constexpr int kPasses = 2;
+    // cos/sin rows of the lane's 8 Q/K items, requested before the tile is staged.
+    struct Pre {
+        u32x4 cs[8][4];
+    };
     QkvOut o;
     // Region of the wave's 128 columns: 0 = Q, 1 = K, 2 = V, -1 = past N.
     __device__ __forceinline__ int region(int nw, int N, int* head) const {
@@ -101,8 +105,25 @@ struct QkvEpi {
                 st_f32(st, m, 32 + l32, pass == 0 ? acc[mb][2][i] : acc[mb][3][i]);
             }
     }
+    // Item t of the lane: staging row (lane + 64 t) / 4, rotation pairs 8 ((lane + 64 t) % 4) ..
+    // + 7 of the pass's 32.
+    __device__ __forceinline__ void prefetch(int pass, int mw, int nw, int lane, int M, int N,
+                                             Pre& pre) const {
+        int head;
+        const int reg = region(nw, N, &head);
+        if (reg != 0 && reg != 1) return;
+#pragma unroll
+        for (int t = 0; t < 8; ++t) {
+            const int id = lane + 64 * t;
+            const int m = min(mw + (id >> 2), M - 1);
+            const int c0 = 32 * pass + 8 * (id & 3);
+            const u32x4* tab = (const u32x4*)(o.rope + (size_t)(m % o.S) * 64 + c0);
+#pragma unroll
+            for (int q = 0; q < 4; ++q) pre.cs[t][q] = tab[q];
+        }
+    }
     __device__ __forceinline__ void flush(int pass, int mw, int nw, int lane, int M, int N,
-                                          const char* st) const {
+                                          const char* st, const Pre& pre) const {
         int head;
         const int reg = region(nw, N, &head);
         if (reg < 0) return;
@@ -134,28 +155,15 @@ struct QkvEpi {
             }
             return;
         }
-        // Q / K: 128 rows x 4 groups of 8 rotation pairs; 8 items per lane, their
-        // cos/sin rows (64 contiguous bytes each) requested before any is used.
-        int rowl[8], sp[8];
-        u32x4 cs[8][4];
+        // Q / K: 128 rows x 4 groups of 8 rotation pairs; 8 items per lane (cos/sin rows from
+        // prefetch()).
 #pragma unroll
         for (int t = 0; t < 8; ++t) {
-            const int id = lane + 64 * t;
-            rowl[t] = id >> 2;
-            const int m = min(mw + rowl[t], M - 1);
-            sp[t] = m % o.S;
-            const int c0 = 32 * pass + 8 * (id & 3);
-            const u32x4* tab = (const u32x4*)(o.rope + (size_t)sp[t] * 64 + c0);
-#pragma unroll
-            for (int q = 0; q < 4; ++q) cs[t][q] = tab[q];
-        }
-#pragma unroll
-        for (int t = 0; t < 8; ++t) {
-            const int id = lane + 64 * t, k = id & 3;
-            const int m = mw + rowl[t];
+            const int id = lane + 64 * t, k = id & 3, rowl = id >> 2;
+            const int m = mw + rowl;
             if (m >= M) continue;
-            const u32x4 a0 = ld_f32(st, rowl[t], 2 * k), a1 = ld_f32(st, rowl[t], 2 * k + 1);
-            const u32x4 b0 = ld_f32(st, rowl[t], 8 + 2 * k), b1 = ld_f32(st, rowl[t], 9 + 2 * k);
+            const u32x4 a0 = ld_f32(st, rowl, 2 * k), a1 = ld_f32(st, rowl, 2 * k + 1);
+            const u32x4 b0 = ld_f32(st, rowl, 8 + 2 * k), b1 = ld_f32(st, rowl, 9 + 2 * k);
             float x1[8], x2[8], c[8], sn[8];
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
@@ -166,8 +174,8 @@ struct QkvEpi {
             }
 #pragma unroll
             for (int e = 0; e < 8; ++e) {
-                c[e] = __uint_as_float(cs[t][e >> 1][2 * (e & 1)]);
-                sn[e] = __uint_as_float(cs[t][e >> 1][2 * (e & 1) + 1]);
+                c[e] = __uint_as_float(pre.cs[t][e >> 1][2 * (e & 1)]);
+                sn[e] = __uint_as_float(pre.cs[t][e >> 1][2 * (e & 1) + 1]);
             }
             u32x4 lo, up;
 #pragma unroll
@@ -183,7 +191,7 @@ struct QkvEpi {
                 dst = o.q + (size_t)m * o.n_q + head * 128;
             } else {
                 const int b = m / o.S;
-                dst = o.kc + (((size_t)b * o.g + head) * o.cap + sp[t]) * 128;
+                dst = o.kc + (((size_t)b * o.g + head) * o.cap + (m - b * o.S)) * 128;
             }
             *(u32x4*)(dst + c0) = lo;
             *(u32x4*)(dst + c0 + 64) = up;
@@ -198,6 +206,10 @@ struct QkvEpi {
 template <bool XF32>
 struct ResidEpi {
     static constexpr int kPasses = 2;
+    // The lane's 16 residual items (row, 8 columns), requested before the tile is staged.
+    struct Pre {
+        u32x4 xv[16][XF32 ? 2 : 1];
+    };
     const void* x;
     uint16_t* y;
     float* yf;
@@ -214,22 +226,26 @@ struct ResidEpi {
                 st_f32(st, m, 32 + l32, pass == 0 ? acc[mb][1][i] : acc[mb][3][i]);
             }
     }
-    __device__ __forceinline__ void flush(int pass, int mw, int nw, int lane, int M, int N,
-                                          const char* st) const {
+    // Item it of the lane: row 8 it + lane / 8, columns 8 (lane % 8) .. + 7 of the pass's 64.
+    __device__ __forceinline__ void prefetch(int pass, int mw, int nw, int lane, int M, int N,
+                                             Pre& pre) const {
         if (nw >= N) return;
-        // 16 items per lane (row, 8 columns); all residual loads are issued first.
-        u32x4 xv[16][XF32 ? 2 : 1];
 #pragma unroll
         for (int it = 0; it < 16; ++it) {
             const int ml = 8 * it + (lane >> 3), c8 = lane & 7;
             const size_t off = (size_t)min(mw + ml, M - 1) * N + nw + 64 * pass + 8 * c8;
             if (XF32) {
-                xv[it][0] = *(const u32x4*)((const float*)x + off);
-                xv[it][XF32 ? 1 : 0] = *(const u32x4*)((const float*)x + off + 4);
+                pre.xv[it][0] = *(const u32x4*)((const float*)x + off);
+                pre.xv[it][XF32 ? 1 : 0] = *(const u32x4*)((const float*)x + off + 4);
             } else {
-                xv[it][0] = *(const u32x4*)((const uint16_t*)x + off);
+                pre.xv[it][0] = *(const u32x4*)((const uint16_t*)x + off);
             }
         }
+    }
+    __device__ __forceinline__ void flush(int pass, int mw, int nw, int lane, int M, int N,
+                                          const char* st, const Pre& pre) const {
+        if (nw >= N) return;
+        const auto& xv = pre.xv;
 #pragma unroll
         for (int it = 0; it < 16; ++it) {
             const int ml = 8 * it + (lane >> 3), c8 = lane & 7;
@@ -387,14 +403,18 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
             load_frags(cur ^ 1, 0, fa, fb);
         }
     }
-    // Epilogue through LDS, in Epi::kPasses passes over the wave's 32 KB.
+    // Epilogue through LDS, in Epi::kPasses passes over the wave's 32 KB.  The pass's global
+    // inputs (cos/sin rows, residual) are requested before the staging, so that their latency
+    // runs under the LDS writes and the barrier.
     char* st = (char*)&lds[0][0][0] + wave * 32768;
 #pragma unroll
     for (int pass = 0; pass < Epi::kPasses; ++pass) {
         __syncthreads();   // the LDS is free: last fragment reads / previous flush are done
+        typename Epi::Pre pre;
+        epi.prefetch(pass, m0 + wm * 128, n0 + wn * 128, lane, M, N, pre);
         epi.stage(pass, acc, m0 + wm * 128, n0 + wn * 128, lane, M, N, st);
         __syncthreads();
-        epi.flush(pass, m0 + wm * 128, n0 + wn * 128, lane, M, N, st);
+        epi.flush(pass, m0 + wm * 128, n0 + wn * 128, lane, M, N, st, pre);
     }
 }
 
