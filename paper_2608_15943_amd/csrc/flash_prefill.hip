@@ -26,7 +26,9 @@
 // Online softmax in the exp2 domain (raw v_exp_f32: arguments never exceed 8,
 // tiny results may flush to 0) with a lazily moved maximum: accumulators
 // are rescaled only when some row's maximum grows by more than 8 (a factor
-// 256), which keeps every exp2 argument <= 8.
+// 256), which keeps every exp2 argument <= 8.  On the tile that holds a wave's diagonal
+// (or the end of the sequence) the 32-key blocks with no visible key skip their
+// QK^T and PV products.
 //
 // Work mapping: hardware workgroup p runs on XCD p % 8 and is the (p / 8)-th
 // dispatched there.  When the B * g (sequence, KV head) groups split evenly
@@ -38,6 +40,7 @@
 // heaviest-first list instead put all the long tiles on the first XCDs: 1.4x
 // slower on the 8-layer stage share.)
 #include <math.h>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -160,13 +163,26 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
         bool issued = false;
 
         const int t0 = t * BKV;
-        if (t0 <= q0w + 31 && q0w < S) {          // some key of the tile is visible to this wave
+        // The tile body; on a tile that holds this wave's diagonal (or the end of the
+        // sequence) the 32-key blocks with no visible key skip their MFMAs.
+        auto body = [&](auto diag_t) {
+            constexpr bool kDiag = decltype(diag_t)::value;
+            int nmb = 4;
+            if constexpr (kDiag) nmb = min(min(4, (q0w + 31 - t0) / 32 + 1), (S - t0 + 31) / 32);
             // ---- S^T = K Q^T: 32 MFMAs, each K fragment read once ------------------------
             f32x16 s[4] = {f32x16{}, f32x16{}, f32x16{}, f32x16{}};
             auto kfrag = [&](int mb, int ks) {
                 const int row = 32 * mb + ksw;
                 return as_bf16x8(lk[stg][row * 16 + ((2 * ks + hi) ^ (row & 15))]);
             };
+            if constexpr (kDiag) {
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+                    if (mb < nmb) {
+#pragma unroll
+                        for (int ks = 0; ks < 8; ++ks) s[mb] = mfma32x32x16(kfrag(mb, ks), qf[ks], s[mb]);
+                    }
+            } else {
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
                 const bf16x8 k0 = kfrag(0, ks), k1 = kfrag(1, ks), k2 = kfrag(2, ks), k3 = kfrag(3, ks);
@@ -175,13 +191,13 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 s[2] = mfma32x32x16(k2, qf[ks], s[2]);
                 s[3] = mfma32x32x16(k3, qf[ks], s[3]);
             }
+            }
             // The next tile goes into the other buffer (read last before the previous barrier)
             // after the K fragment reads of this one, not in the same burst (1-2 % faster).
             if (more) issue_tile(t + 1, stg ^ 1);
             issued = true;
             // Register i of block mb holds position t0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
-            const bool diag = (t0 + BKV - 1 > q0w) || (t0 + BKV > S);
-            if (diag) {
+            if constexpr (kDiag) {
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
@@ -228,6 +244,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 const int mb = c >> 1, p = c & 1;
+                if (kDiag && mb >= nmb) continue;
 #pragma unroll
                 for (int db = 0; db < 4; ++db) {
                     const int d = 32 * db + l32;
@@ -235,6 +252,10 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                     o[db] = mfma32x32x16(vf, pb[mb][p], o[db]);
                 }
             }
+        };
+        if (t0 <= q0w + 31 && q0w < S) {          // some key of the tile is visible to this wave
+            if ((t0 + BKV - 1 > q0w) || (t0 + BKV > S)) body(std::true_type{});
+            else body(std::false_type{});
         }
         if (more && !issued) issue_tile(t + 1, stg ^ 1);   // this wave saw no key of tile t
         // One barrier: tile t + 1 has landed in LDS (every wave waited for its own loads)

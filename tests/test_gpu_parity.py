@@ -161,6 +161,7 @@ def test_decode_fp32_tiny():
     (512, 4, 2, [0, 0, 0], [300, 1000, 257], 1024),           # r=2, several splits
     (1024, 8, 8, [0, 1], [2000], 2048),                       # MHA
     (512, 4, 1, [0, 0], [5000, 3, 4095], 5120),                # ragged, > 1 split
+    (512, 4, 2, [0, 0, 2], [127, 0, 64, 1], 128),             # new token in the slot's last position
 ])
 def test_decode_bf16(h, a, g, tau, lens, cap):
     w = small_workload(f"dec-h{h}-a{a}-g{g}", len(tau), h, a, g, tau)
