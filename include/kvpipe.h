@@ -8,8 +8,9 @@
  * against its producer's cache.  It runs as a causal prefill / training
  * forward over S tokens and as a single-token decode step over a long cache.
  * A CPU planner implements the paper's offline FIR-balancing rule
- * (Sec. 2.3-2.7, Algorithm 1; App. A.3 guardrail; App. A.7 FLOPs model) and
- * can produce the sharing map.
+ * (Sec. 2.3-2.7, Algorithm 1; App. A.3 guardrail; App. A.7 FLOPs model), the
+ * two position-based placement archetypes it is compared with (Sec. 2.5),
+ * and can produce the sharing map.
  *
  * Conventions
  * -----------
@@ -78,6 +79,9 @@ extern "C" {
 #define KVP_STOP_FIR_MET        0  /* FIR <= 1 + eps                                    */
 #define KVP_STOP_BUDGET         1  /* m conversions made                                */
 #define KVP_STOP_NO_CONVERTIBLE 2  /* the chosen stage has no admissible full layer left */
+
+#define KVP_PLACE_UNIFORM           0  /* Sec. 2.5, Uniform split             */
+#define KVP_PLACE_SYMMETRIC_BIPOLAR 1  /* Sec. 2.5, Symmetric Bipolar split   */
 
 /* ======================================================================== */
 /* Planner (host only; touches no GPU)                                       */
@@ -157,6 +161,53 @@ typedef struct kvp_plan_out {
  * F(0) - F(1) <= 0 for an admissible layer.
  */
 int kvp_plan_fir(const kvp_plan_in* in, kvp_plan_out* out);
+
+/*
+ * kvp_stage_flops -- Eq. (stage_flops_z): stage_flops[i] = the sum of F_l(z_l)
+ * over the layers l of stage i (left to right), plus f_lmhead on stage P-1,
+ * in the order kvp_plan_fir uses.  Arrays are caller-owned: stage_of_layer,
+ * f_full, f_share, z of length L; stage_flops of length P (written).
+ * Errors: KVP_E_INVALID_ARG on NULL arrays, L < 1, P < 1, P > L or a stage
+ * index outside 0..P-1.
+ */
+int kvp_stage_flops(int L, int P, const int32_t* stage_of_layer, const double* f_full,
+                    const double* f_share, const uint8_t* z, double f_lmhead,
+                    double* stage_flops);
+
+/*
+ * kvp_place -- the two position-based placement archetypes of Sec. 2.5.
+ * They place k conversions without looking at FLOPs (the FLOPs-driven
+ * Architecture-Balanced archetype is kvp_plan_fir); the caller evaluates the
+ * result with kvp_stage_flops and kvp_fir (Table 2).
+ *
+ * KVP_PLACE_UNIFORM: the k conversions are spaced evenly over the layers of
+ *   the last min(k, P) stages, the first on the last layer, moving left:
+ *   target_j = hi - round(j (hi - lo) / (k - 1)), halves rounded up, with
+ *   hi = L - 1 and lo the first layer of stage P - min(k, P).  With equal
+ *   stages and k <= P this is one conversion in each of the last k stages
+ *   (App. A.1 Table A1; for LLaMA2-7B on 8 stages and k = 4 the 1-indexed
+ *   layers 17, 22, 27, 32 of App. A.4).
+ * KVP_PLACE_SYMMETRIC_BIPOLAR: two anchors, the last layer of stage P-1 and
+ *   the last layer of the middle stage (P-1)/2; conversions alternate between
+ *   them, the last stage first, each anchor moving left from its previous
+ *   choice (App. A.1 Table A2: two each in stages 3 and 7 for k = 4, P = 8).
+ *   An anchor with no free layer left hands its turns to the other; with
+ *   P = 1 the anchors coincide.
+ * Under both, a layer is free when it is admissible (the caller mask, the
+ * App. A.3 guardrail alpha as in kvp_plan_fir, never layer 0) and not yet
+ * converted; a Uniform target that is not free moves to the nearest free
+ * layer on its left, else on its right.
+ * In: stage_of_layer[L] as in kvp_plan_in; admissible[L] or NULL; k >= 0.
+ * Out: z[L] (1 = KV-sharing layer), *n_placed, *stop_reason =
+ * KVP_STOP_BUDGET when all k were placed, else KVP_STOP_NO_CONVERTIBLE
+ * (no free layer was left).  Integer arithmetic only.
+ * Errors: KVP_E_INVALID_ARG on NULL pointers, L < 1, P < 1, P > L, k < 0,
+ * an unknown strategy, or a partition that is not 0..P-1, non-decreasing
+ * and without empty stages.
+ */
+int kvp_place(int strategy, int L, int P, const int32_t* stage_of_layer, int k,
+              const uint8_t* admissible, double alpha, uint8_t* z, int32_t* n_placed,
+              int32_t* stop_reason);
 
 /*
  * kvp_map_from_mask -- Eq. (3) with tau(l) = nearest earlier full-attention

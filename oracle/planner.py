@@ -1,7 +1,8 @@
 """Oracle for the offline KV-Pipe planner (test infrastructure only).
 
-Follows Sec. 2.3-2.7 (FIR, stage FLOPs under z, Algorithm 1), App. A.3 (the
-safe-layer guardrail) and App. A.7 (attention FLOPs under MHA/GQA).
+Follows Sec. 2.3-2.7 (FIR, stage FLOPs under z, the Uniform and Symmetric
+Bipolar placements, Algorithm 1), App. A.3 (the safe-layer guardrail) and
+App. A.7 (attention FLOPs under MHA/GQA).
 
 Floating-point order is fixed so that a compiled planner doing the same IEEE
 double operations in the same order reaches the same mask bit for bit:
@@ -192,6 +193,124 @@ def plan_fir(stage_of_layer: Sequence[int], P: int, f_full: Sequence[float],
         trace.append(cur)
     return PlanResult(z=z, stage_flops=F, fir=cur, n_converted=t, stop_reason=stop,
                       fir_trace=trace)
+
+
+# ---------------------------------------------------------------------------
+# Sec. 2.5: the Uniform and Symmetric Bipolar placement archetypes.  Neither
+# looks at FLOPs: each places a fixed number k of conversions by position.
+# ---------------------------------------------------------------------------
+
+def _placement_admissible(stage_of_layer: Sequence[int], P: int,
+                          admissible: Optional[Sequence[bool]], alpha: float) -> List[bool]:
+    """Caller mask, then the App. A.3 guardrail; layer 0 (no prior layer) never."""
+    L = len(stage_of_layer)
+    if L < 1 or P < 1 or P > L:
+        raise ValueError("need 1 <= P <= L")
+    if stage_of_layer[0] != 0 or stage_of_layer[-1] != P - 1 or any(
+            not 0 <= b - a <= 1 for a, b in zip(stage_of_layer, stage_of_layer[1:])):
+        raise ValueError("stages must be contiguous, 0..P-1, none empty")
+    ok = [True] * L if admissible is None else [bool(x) for x in admissible]
+    if alpha >= 0.0:
+        ok = [x and y for x, y in zip(ok, guardrail_admissible(L, alpha))]
+    ok[0] = False
+    return ok
+
+
+def place_uniform(stage_of_layer: Sequence[int], P: int, k: int,
+                  admissible: Optional[Sequence[bool]] = None, alpha: float = -1.0):
+    """Uniform split: k conversions spread evenly, anchored at the last layer.
+
+    Reading (the paper gives the rule in words and one example): the k
+    conversions are spaced evenly over the layers of the last min(k, P)
+    stages, the first at the last layer, moving left:
+    target_j = hi - round(j (hi - lo) / (k - 1)), j = 0 .. k-1, with hi the
+    last layer, lo the first layer of stage P - min(k, P) and halves rounded
+    up.  With equal stages and k <= P this is one conversion in each of the
+    last k stages.  A target that is not admissible or already taken moves
+    to the nearest free admissible layer on its left, else on its right.
+    Returns (z, n placed, stop reason).
+    """
+    ok = _placement_admissible(stage_of_layer, P, admissible, alpha)
+    if k < 0:
+        raise ValueError("k must be >= 0")
+    L = len(stage_of_layer)
+    z = [0] * L
+    c = min(k, P)
+    hi = L - 1
+    lo = next(l for l in range(L) if stage_of_layer[l] >= P - c) if c else hi
+    n = 0
+    for j in range(k):
+        t = hi if k == 1 else hi - (2 * j * (hi - lo) + (k - 1)) // (2 * (k - 1))
+        free = [l for l in range(L) if ok[l] and not z[l]]
+        left = [l for l in free if l <= t]
+        right = [l for l in free if l > t]
+        if left:
+            z[max(left)] = 1
+        elif right:
+            z[min(right)] = 1
+        else:
+            return z, n, STOP_NO_CONVERTIBLE
+        n += 1
+    return z, n, STOP_BUDGET
+
+
+def place_symmetric_bipolar(stage_of_layer: Sequence[int], P: int, k: int,
+                            admissible: Optional[Sequence[bool]] = None, alpha: float = -1.0):
+    """Symmetric Bipolar split: two anchors, each moving left.
+
+    Reading: the anchors are the last layer of the last stage and the last
+    layer of the middle stage floor((P - 1) / 2) (stage 3 of 8, as in
+    App. A.1, Table A2).  Conversions alternate between the anchors,
+    the last stage first; each anchor converts the nearest free admissible
+    layer at or left of its previous choice.  An anchor with nothing left
+    hands its turns to the other; with P = 1 the two anchors coincide.
+    Returns (z, n placed, stop reason).
+    """
+    ok = _placement_admissible(stage_of_layer, P, admissible, alpha)
+    if k < 0:
+        raise ValueError("k must be >= 0")
+    L = len(stage_of_layer)
+    mid = (P - 1) // 2
+    last_of_mid = max(l for l in range(L) if stage_of_layer[l] == mid)
+    cursors = [L - 1] if mid == P - 1 else [L - 1, last_of_mid]
+    z = [0] * L
+    n = 0
+    turn = 0
+    while n < k:
+        placed = False
+        for attempt in range(len(cursors)):
+            a = (turn + attempt) % len(cursors)
+            l = cursors[a]
+            while l >= 0 and not (ok[l] and not z[l]):
+                l -= 1
+            cursors[a] = l
+            if l >= 0:
+                z[l] = 1
+                cursors[a] = l - 1
+                placed = True
+                break
+        if not placed:
+            return z, n, STOP_NO_CONVERTIBLE
+        n += 1
+        turn = (turn + 1) % len(cursors)
+    return z, n, STOP_BUDGET
+
+
+def strategy_table(stage_of_layer: Sequence[int], P: int, f_full: Sequence[float],
+                   f_share: Sequence[float], f_lmhead: float, k: int, eps: float):
+    """The comparison of Sec. 2.7 (Table 2): Baseline, Uniform, Symmetric
+    Bipolar and Architecture-Balanced (Algorithm 1 with budget m = k), each
+    as (name, z, stage FLOPs, FIR)."""
+    rows = []
+    z0 = [0] * len(stage_of_layer)
+    for name, z in (("baseline", z0),
+                    ("uniform", place_uniform(stage_of_layer, P, k)[0]),
+                    ("symmetric_bipolar", place_symmetric_bipolar(stage_of_layer, P, k)[0])):
+        F = stage_flops(stage_of_layer, P, f_full, f_share, z, f_lmhead)
+        rows.append((name, z, F, fir(F)))
+    res = plan_fir(stage_of_layer, P, f_full, f_share, f_lmhead, eps, m=k)
+    rows.append(("arch_balanced", res.z, res.stage_flops, res.fir))
+    return rows
 
 
 # ---------------------------------------------------------------------------

@@ -31,9 +31,12 @@ KVP_PHASE_DECODE = 1
 KVP_STOP_FIR_MET = 0
 KVP_STOP_BUDGET = 1
 KVP_STOP_NO_CONVERTIBLE = 2
+KVP_PLACE_UNIFORM = 0
+KVP_PLACE_SYMMETRIC_BIPOLAR = 1
 
 EXPORTS = [
-    "kvp_layer_flops", "kvp_fir", "kvp_plan_fir", "kvp_map_from_mask", "kvp_canonicalize_map",
+    "kvp_layer_flops", "kvp_fir", "kvp_plan_fir", "kvp_stage_flops", "kvp_place",
+    "kvp_map_from_mask", "kvp_canonicalize_map",
     "kvp_create", "kvp_destroy", "kvp_set_layer", "kvp_set_kv_slot", "kvp_workspace_size",
     "kvp_prefill", "kvp_layer_forward", "kvp_decode_step", "kvp_get_map", "kvp_status_string",
     "kvp_last_error", "kvp_profile_enable", "kvp_profile_read",
@@ -91,6 +94,10 @@ def lib() -> C.CDLL:
         "kvp_layer_flops": ([C.POINTER(kvp_shape), i32, C.POINTER(dbl), C.POINTER(dbl)], i32),
         "kvp_fir": ([i32, C.POINTER(dbl), C.POINTER(dbl)], i32),
         "kvp_plan_fir": ([C.POINTER(kvp_plan_in), C.POINTER(kvp_plan_out)], i32),
+        "kvp_stage_flops": ([i32, i32, C.POINTER(C.c_int32), C.POINTER(dbl), C.POINTER(dbl),
+                             C.POINTER(C.c_uint8), dbl, C.POINTER(dbl)], i32),
+        "kvp_place": ([i32, i32, i32, C.POINTER(C.c_int32), i32, C.POINTER(C.c_uint8), dbl,
+                       C.POINTER(C.c_uint8), C.POINTER(C.c_int32), C.POINTER(C.c_int32)], i32),
         "kvp_map_from_mask": ([i32, C.POINTER(C.c_uint8), C.POINTER(C.c_int32)], i32),
         "kvp_canonicalize_map": ([i32, C.POINTER(C.c_int32), C.POINTER(C.c_int32)], i32),
         "kvp_create": ([C.POINTER(kvp_model_desc), C.POINTER(C.c_int32), C.POINTER(vp)], i32),
@@ -169,6 +176,29 @@ def kvp_plan_fir(stage_of_layer, f_full, f_share, f_lmhead, eps, m=0, admissible
     _check(lib().kvp_plan_fir(C.byref(pin), C.byref(pout)), "kvp_plan_fir")
     return dict(z=list(z), stage_flops=list(F), fir=pout.fir, n_converted=pout.n_converted,
                 stop_reason=pout.stop_reason)
+
+
+def kvp_stage_flops(stage_of_layer, f_full, f_share, z, f_lmhead, P=None):
+    """Eq. (stage_flops_z): per-stage FLOPs of a mask, LM head on the last stage."""
+    L = len(stage_of_layer)
+    P = (max(stage_of_layer) + 1) if P is None else P
+    F = (C.c_double * P)()
+    _check(lib().kvp_stage_flops(L, P, _i32(stage_of_layer), _f64(f_full), _f64(f_share),
+                                 (C.c_uint8 * L)(*[1 if x else 0 for x in z]), float(f_lmhead), F),
+           "kvp_stage_flops")
+    return list(F)
+
+
+def kvp_place(strategy, stage_of_layer, k, admissible=None, alpha=-1.0, P=None):
+    """Sec. 2.5 Uniform / Symmetric Bipolar placement; returns (z, n_placed, stop_reason)."""
+    L = len(stage_of_layer)
+    P = (max(stage_of_layer) + 1) if P is None else P
+    adm = None if admissible is None else (C.c_uint8 * L)(*[1 if x else 0 for x in admissible])
+    z = (C.c_uint8 * L)()
+    n, stop = C.c_int32(), C.c_int32()
+    _check(lib().kvp_place(int(strategy), L, P, _i32(stage_of_layer), int(k), adm, float(alpha), z,
+                           C.byref(n), C.byref(stop)), "kvp_place")
+    return list(z), n.value, stop.value
 
 
 def kvp_map_from_mask(z: Sequence[int]):

@@ -1,6 +1,7 @@
 // Offline KV-Pipe planner: App. A.7 FLOPs model, the FIR metric
 // (Eqs. flop_imbalance_main, favg), stage FLOPs under a mask (Eq. stage_flops_z),
-// Algorithm 1 with the App. A.3 guardrail, and the mask -> producer map.
+// the Uniform and Symmetric Bipolar placements (Sec. 2.5), Algorithm 1 with the
+// App. A.3 guardrail, and the mask -> producer map.
 //
 // Host code only.  Built with -ffp-contract=off and without fast-math so that
 // every double operation rounds exactly as written: the mask must not depend
@@ -36,6 +37,92 @@ double max_of(const std::vector<double>& F) {
     for (double v : F)
         if (v > m) m = v;
     return m;
+}
+
+// The partition: non-decreasing, starts at stage 0, ends at P-1, no stage skipped.
+bool valid_partition(int L, int P, const int32_t* stage_of_layer) {
+    if (stage_of_layer[0] != 0 || stage_of_layer[L - 1] != P - 1) return false;
+    for (int l = 1; l < L; ++l) {
+        const int dlt = stage_of_layer[l] - stage_of_layer[l - 1];
+        if (dlt < 0 || dlt > 1) return false;
+    }
+    return true;
+}
+
+// Admissible layers: caller mask, then the App. A.3 guardrail, never layer 0.
+std::vector<uint8_t> admissible_layers(int L, const uint8_t* mask, double alpha) {
+    std::vector<uint8_t> adm(L, 1);
+    if (mask)
+        for (int l = 0; l < L; ++l) adm[l] = mask[l] ? 1 : 0;
+    if (alpha >= 0.0) {
+        const double lo = std::ceil(alpha * static_cast<double>(L));
+        for (int l = 0; l < L; ++l)
+            if (!(static_cast<double>(l + 1) >= lo)) adm[l] = 0;
+    }
+    adm[0] = 0;
+    return adm;
+}
+
+// Uniform: k targets spaced evenly from the last layer leftward over the layers of the
+// last min(k, P) stages (rounded half up); a target that is not free moves to the nearest
+// free admissible layer on its left, else on its right.
+int place_uniform(int L, int P, const int32_t* stage_of_layer, int k,
+                  const std::vector<uint8_t>& adm, std::vector<uint8_t>& z) {
+    const int c = k < P ? k : P;
+    const int hi = L - 1;
+    int lo = hi;
+    if (c > 0)
+        for (int l = 0; l < L; ++l)
+            if (stage_of_layer[l] >= P - c) { lo = l; break; }
+    int n = 0;
+    for (int j = 0; j < k; ++j) {
+        const int64_t span = hi - lo;
+        const int t = k == 1 ? hi
+                             : hi - static_cast<int>((2 * j * span + (k - 1)) / (2 * static_cast<int64_t>(k - 1)));
+        int pick = -1;
+        for (int l = t; l >= 0; --l)
+            if (adm[l] && !z[l]) { pick = l; break; }
+        if (pick < 0)
+            for (int l = t + 1; l < L; ++l)
+                if (adm[l] && !z[l]) { pick = l; break; }
+        if (pick < 0) break;
+        z[pick] = 1;
+        ++n;
+    }
+    return n;
+}
+
+// Symmetric Bipolar: anchors at the last layer of the last stage and of the middle stage
+// (P - 1) / 2; conversions alternate between them, last stage first, each anchor taking the
+// nearest free admissible layer at or left of its previous choice.  An exhausted anchor
+// hands its turns to the other; with P = 1 there is one anchor.
+int place_symmetric(int L, int P, const int32_t* stage_of_layer, int k,
+                    const std::vector<uint8_t>& adm, std::vector<uint8_t>& z) {
+    const int mid = (P - 1) / 2;
+    int last_of_mid = 0;
+    for (int l = 0; l < L; ++l)
+        if (stage_of_layer[l] == mid) last_of_mid = l;
+    int cur[2] = {L - 1, last_of_mid};
+    const int na = mid == P - 1 ? 1 : 2;
+    int n = 0, turn = 0;
+    while (n < k) {
+        bool placed = false;
+        for (int att = 0; att < na && !placed; ++att) {
+            const int a = (turn + att) % na;
+            int l = cur[a];
+            while (l >= 0 && !(adm[l] && !z[l])) --l;
+            cur[a] = l;
+            if (l >= 0) {
+                z[l] = 1;
+                cur[a] = l - 1;
+                placed = true;
+            }
+        }
+        if (!placed) break;
+        ++n;
+        turn = (turn + 1) % na;
+    }
+    return n;
 }
 
 }  // namespace
@@ -89,25 +176,10 @@ extern "C" int kvp_plan_fir(const kvp_plan_in* in, kvp_plan_out* out) {
     if (L < 1 || P < 1 || P > L) return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: need 1 <= P <= L");
     if (!(in->eps > 0.0)) return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: eps must be > 0");
     if (!(in->f_lmhead >= 0.0)) return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: f_lmhead must be >= 0");
-    // The partition: non-decreasing, starts at stage 0, ends at P-1, no stage skipped.
-    if (in->stage_of_layer[0] != 0 || in->stage_of_layer[L - 1] != P - 1)
-        return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: stages must run from 0 to P-1");
-    for (int l = 1; l < L; ++l) {
-        const int dlt = in->stage_of_layer[l] - in->stage_of_layer[l - 1];
-        if (dlt < 0 || dlt > 1)
-            return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: stage_of_layer must be non-decreasing "
-                                           "with no empty stage");
-    }
-    // Admissible layers: caller mask, then the guardrail, never layer 0.
-    std::vector<uint8_t> adm(L, 1);
-    if (in->admissible)
-        for (int l = 0; l < L; ++l) adm[l] = in->admissible[l] ? 1 : 0;
-    if (in->alpha >= 0.0) {
-        const double lo = std::ceil(in->alpha * static_cast<double>(L));
-        for (int l = 0; l < L; ++l)
-            if (!(static_cast<double>(l + 1) >= lo)) adm[l] = 0;
-    }
-    adm[0] = 0;
+    if (!valid_partition(L, P, in->stage_of_layer))
+        return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: stage_of_layer must run from 0 to P-1, "
+                                       "non-decreasing, with no empty stage");
+    const std::vector<uint8_t> adm = admissible_layers(L, in->admissible, in->alpha);
     for (int l = 0; l < L; ++l)
         if (adm[l] && !(in->f_full[l] - in->f_share[l] > 0.0))
             return fail(KVP_E_INVALID_ARG, "kvp_plan_fir: F(0) - F(1) must be > 0 for every "
@@ -147,6 +219,56 @@ extern "C" int kvp_plan_fir(const kvp_plan_in* in, kvp_plan_out* out) {
     out->fir = cur;
     out->n_converted = t;
     out->stop_reason = stop;
+    return ok();
+}
+
+extern "C" int kvp_stage_flops(int L, int P, const int32_t* stage_of_layer, const double* f_full,
+                               const double* f_share, const uint8_t* z, double f_lmhead,
+                               double* stage_flops) {
+    using namespace kvp;
+    if (!stage_of_layer || !f_full || !f_share || !z || !stage_flops)
+        return fail(KVP_E_INVALID_ARG, "kvp_stage_flops: NULL pointer");
+    if (L < 1 || P < 1 || P > L) return fail(KVP_E_INVALID_ARG, "kvp_stage_flops: need 1 <= P <= L");
+    for (int l = 0; l < L; ++l)
+        if (stage_of_layer[l] < 0 || stage_of_layer[l] >= P)
+            return fail(KVP_E_INVALID_ARG, "kvp_stage_flops: stage index out of range");
+    kvp_plan_in in{};
+    in.L = L;
+    in.P = P;
+    in.stage_of_layer = stage_of_layer;
+    in.f_full = f_full;
+    in.f_share = f_share;
+    in.f_lmhead = f_lmhead;
+    std::vector<uint8_t> zz(z, z + L);
+    std::vector<double> F;
+    stage_sums(in, zz, F);
+    std::memcpy(stage_flops, F.data(), sizeof(double) * P);
+    return ok();
+}
+
+extern "C" int kvp_place(int strategy, int L, int P, const int32_t* stage_of_layer, int k,
+                         const uint8_t* admissible, double alpha, uint8_t* z, int32_t* n_placed,
+                         int32_t* stop_reason) {
+    using namespace kvp;
+    if (!stage_of_layer || !z || !n_placed || !stop_reason)
+        return fail(KVP_E_INVALID_ARG, "kvp_place: NULL pointer");
+    if (L < 1 || P < 1 || P > L) return fail(KVP_E_INVALID_ARG, "kvp_place: need 1 <= P <= L");
+    if (k < 0) return fail(KVP_E_INVALID_ARG, "kvp_place: k must be >= 0");
+    if (!valid_partition(L, P, stage_of_layer))
+        return fail(KVP_E_INVALID_ARG, "kvp_place: stage_of_layer must run from 0 to P-1, "
+                                       "non-decreasing, with no empty stage");
+    const std::vector<uint8_t> adm = admissible_layers(L, admissible, alpha);
+    std::vector<uint8_t> zz(L, 0);
+    int n;
+    if (strategy == KVP_PLACE_UNIFORM)
+        n = place_uniform(L, P, stage_of_layer, k, adm, zz);
+    else if (strategy == KVP_PLACE_SYMMETRIC_BIPOLAR)
+        n = place_symmetric(L, P, stage_of_layer, k, adm, zz);
+    else
+        return fail(KVP_E_INVALID_ARG, "kvp_place: unknown strategy %d", strategy);
+    std::memcpy(z, zz.data(), L);
+    *n_placed = n;
+    *stop_reason = n == k ? KVP_STOP_BUDGET : KVP_STOP_NO_CONVERTIBLE;
     return ok();
 }
 

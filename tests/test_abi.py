@@ -117,6 +117,71 @@ def test_planner_rejections():
         kb.kvp_plan_fir([0], [1], [0.5], 0, eps=0.1, P=2)
 
 
+def _random_partition(rng, L, P):
+    cuts = sorted(rng.sample(range(1, L), P - 1)) if P > 1 else []
+    return [sum(1 for c in cuts if l >= c) for l in range(L)]
+
+
+def test_placements_match_oracle():
+    rng = random.Random(99)
+    fns = {kb.KVP_PLACE_UNIFORM: opl.place_uniform,
+           kb.KVP_PLACE_SYMMETRIC_BIPOLAR: opl.place_symmetric_bipolar}
+    for _ in range(400):
+        L = rng.randint(1, 48)
+        P = rng.randint(1, min(L, 12))
+        stage = _random_partition(rng, L, P) if rng.random() < 0.5 else [l * P // L for l in range(L)]
+        k = rng.randint(0, L + 2)
+        adm = [rng.random() < 0.75 for _ in range(L)] if rng.random() < 0.4 else None
+        alpha = rng.choice([-1.0, 0.0, 0.3, 0.5, 0.95])
+        for strat, fn in fns.items():
+            ref = fn(stage, P, k, admissible=adm, alpha=alpha)
+            got = kb.kvp_place(strat, stage, k, admissible=adm, alpha=alpha, P=P)
+            assert got == (ref[0], ref[1], ref[2]), (strat, stage, k, adm, alpha)
+
+
+def test_stage_flops_matches_oracle():
+    rng = random.Random(7)
+    for _ in range(100):
+        L = rng.randint(1, 40)
+        P = rng.randint(1, L)
+        stage = _random_partition(rng, L, P)
+        ff = [rng.uniform(1e9, 1e12) for _ in range(L)]
+        fs = [f * rng.uniform(0.5, 0.99) for f in ff]
+        z = [rng.randint(0, 1) for _ in range(L)]
+        lm = rng.uniform(0, 5e12)
+        assert kb.kvp_stage_flops(stage, ff, fs, z, lm, P=P) == opl.stage_flops(stage, P, ff, fs, z, lm)
+
+
+def test_fir_table_reproducer_table2():
+    """The FIR-table reproducer (C++ planner) against the oracle's strategy table and
+    the FIRs Table 2 prints for LLaMA2-7B, PP = 8, S = 8K, 4 KV-sharing layers."""
+    from paper_2608_15943_amd.fir_table import fir_table
+    rows = {r["strategy"]: r for r in fir_table(eps=1e-4)}
+    stage = [l // 4 for l in range(32)]
+    f0, f1 = opl.layer_flops_prefill(1, 8192, 4096, 32, 32, ffn=11008)
+    ref = opl.strategy_table(stage, 8, [f0] * 32, [f1] * 32, opl.mm_flops(8192, 4096, 32000), 4, 1e-4)
+    for name, z, F, f in ref:
+        assert rows[name]["layers"] == [l + 1 for l in range(32) if z[l]]
+        assert rows[name]["stage_flops"] == F and rows[name]["fir"] == f
+    printed = {"baseline": (1.119453925, 1e-9), "uniform": (1.103804831, 4e-5),
+               "symmetric_bipolar": (1.068260764, 4e-5), "arch_balanced": (1.00040391, 2e-5)}
+    for name, (v, tol) in printed.items():
+        assert abs(rows[name]["fir"] - v) < tol, name
+    assert rows["uniform"]["layers"] == [17, 22, 27, 32]
+
+
+def test_placement_rejections():
+    for args in ((7, [0, 1], 1), (kb.KVP_PLACE_UNIFORM, [0, 1], -1),
+                 (kb.KVP_PLACE_UNIFORM, [0, 1, 0], 1), (kb.KVP_PLACE_SYMMETRIC_BIPOLAR, [0, 2, 2], 1)):
+        with pytest.raises(kb.KvpError) as e:
+            kb.kvp_place(*args)
+        assert e.value.code == kb.KVP_E_INVALID_ARG
+    with pytest.raises(kb.KvpError):        # P > L
+        kb.kvp_place(kb.KVP_PLACE_UNIFORM, [0], 1, P=2)
+    with pytest.raises(kb.KvpError):        # stage index out of range
+        kb.kvp_stage_flops([0, 3], [1.0, 1.0], [0.5, 0.5], [0, 0], 0.0, P=2)
+
+
 def test_maps():
     assert kb.kvp_map_from_mask([0, 0, 0, 0, 0, 1, 0, 1]) == [0, 1, 2, 3, 4, 4, 6, 6]
     assert kb.kvp_map_from_mask([0, 1, 1, 1]) == opl.map_from_mask([0, 1, 1, 1])

@@ -102,6 +102,150 @@ def test_uniform_and_symmetric_placements_tables_a1_a2_and_table2():
     assert abs(pl.fir(F) - float(g["table2_fir_symmetric"])) < 4e-5
 
 
+def per_stage(stage, z, P):
+    c = [0] * P
+    for l, zl in enumerate(z):
+        c[stage[l]] += zl
+    return c
+
+
+def test_uniform_rule_reproduces_printed_layers_and_table_a1():
+    g = golden()
+    stage, ff, fs, lm = llama2_7b(8192, 8)
+    z, n, stop = pl.place_uniform(stage, 8, 4)
+    assert [l + 1 for l in range(L) if z[l]] == [int(x) for x in g["layers_uniform"].split(",")]
+    assert per_stage(stage, z, 8) == [int(x) for x in g["tableA1_uniform_shared_per_stage"].split(",")]
+    assert n == 4 and stop == pl.STOP_BUDGET
+    F = pl.stage_flops(stage, 8, ff, fs, z, lm)
+    assert f"{F[5]:.2E}" == g["tableA1_uniform_stage_flops_shared1"]
+    assert abs(pl.fir(F) - float(g["table2_fir_uniform"])) < 4e-5
+
+
+def test_symmetric_rule_reproduces_table_a2():
+    g = golden()
+    stage, ff, fs, lm = llama2_7b(8192, 8)
+    z, n, stop = pl.place_symmetric_bipolar(stage, 8, 4)
+    assert per_stage(stage, z, 8) == [int(x) for x in g["tableA2_symmetric_shared_per_stage"].split(",")]
+    assert [l + 1 for l in range(L) if z[l]] == [15, 16, 31, 32]      # tail-most of stages 3, 7
+    assert n == 4 and stop == pl.STOP_BUDGET
+    F = pl.stage_flops(stage, 8, ff, fs, z, lm)
+    assert abs(pl.fir(F) - float(g["table2_fir_symmetric"])) < 4e-5
+    # The sensitivity table's layer set (stages 4 and 7) has the same stage-FLOPs
+    # multiset, so the two printed descriptions agree on the FIR.
+    z2 = [0] * L
+    for l in (int(x) for x in g["layers_symmetric_sensitivity"].split(",")):
+        z2[l - 1] = 1
+    F2 = pl.stage_flops(stage, 8, ff, fs, z2, lm)
+    assert sorted(F2) == sorted(F)
+    assert abs(pl.fir(F2) - pl.fir(F)) < 1e-15
+
+
+def test_strategy_table_reproduces_table2_and_table_a3():
+    g = golden()
+    stage, ff, fs, lm = llama2_7b(8192, 8)
+    rows = {name: (z, F, f) for name, z, F, f in pl.strategy_table(stage, 8, ff, fs, lm, k=4, eps=1e-4)}
+    assert abs(rows["baseline"][2] - float(g["table2_fir_baseline"])) < 1e-9
+    assert abs(rows["uniform"][2] - float(g["table2_fir_uniform"])) < 4e-5
+    assert abs(rows["symmetric_bipolar"][2] - float(g["table2_fir_symmetric"])) < 4e-5
+    assert abs(rows["arch_balanced"][2] - float(g["table2_fir_arch_balanced"])) < 2e-5
+    assert per_stage(stage, rows["arch_balanced"][0], 8) == [
+        int(x) for x in g["tableA3_arch_shared_per_stage"].split(",")]
+    # The paper's ranking: each archetype closer to 1 than the one before.
+    f = [rows[k][2] for k in ("baseline", "uniform", "symmetric_bipolar", "arch_balanced")]
+    assert f == sorted(f, reverse=True)
+    # Same budget, same total FLOPs removed: only where they are removed differs.
+    tot = {k: sum(v[1]) for k, v in rows.items()}
+    assert len({tot["uniform"], tot["symmetric_bipolar"], tot["arch_balanced"]}) == 1
+
+
+# Toy partition for the placements: 12 layers, stages {0-2},{3-5},{6-8},{9-11}.
+def test_uniform_toys():
+    T = [l // 3 for l in range(12)]
+    on = lambda z: [l for l in range(len(z)) if z[l]]
+    # k = 2: span = stages 2-3 = layers 6..11, targets 11 and 11 - round(5) = 6.
+    assert on(pl.place_uniform(T, 4, 2)[0]) == [6, 11]
+    # k = 4: span = all, targets 11, 11 - round(11/3) = 7, 11 - round(22/3) = 4, 0;
+    # layer 0 is never converted, so its target moves right to layer 1.
+    assert on(pl.place_uniform(T, 4, 4)[0]) == [1, 4, 7, 11]
+    # k = 1: the last layer; k = 0: nothing.
+    assert on(pl.place_uniform(T, 4, 1)[0]) == [11]
+    assert pl.place_uniform(T, 4, 0) == ([0] * 12, 0, pl.STOP_BUDGET)
+    # More than the 11 convertible layers: all of them, then stop.
+    z, n, stop = pl.place_uniform(T, 4, 12)
+    assert on(z) == list(range(1, 12)) and n == 11 and stop == pl.STOP_NO_CONVERTIBLE
+    # Guardrail alpha = 0.5: 1-indexed layers >= 6 (0-indexed >= 5).  Targets 11, 7, 4, 0:
+    # 4 and 0 have no free layer on their left and move right to 5 and 6.
+    assert on(pl.place_uniform(T, 4, 4, alpha=0.5)[0]) == [5, 6, 7, 11]
+    # One stage: span = all five layers, targets 4 and 0 -> 1.
+    assert on(pl.place_uniform([0] * 5, 1, 2)[0]) == [1, 4]
+
+
+def test_symmetric_toys():
+    T = [l // 3 for l in range(12)]
+    on = lambda z: [l for l in range(len(z)) if z[l]]
+    # Anchors: layer 11 (last stage) and layer 5 (last of stage (4 - 1) // 2 = 1).
+    assert on(pl.place_symmetric_bipolar(T, 4, 1)[0]) == [11]
+    assert on(pl.place_symmetric_bipolar(T, 4, 3)[0]) == [5, 10, 11]
+    assert on(pl.place_symmetric_bipolar(T, 4, 7)[0]) == [3, 4, 5, 8, 9, 10, 11]
+    # Guardrail alpha = 0.5 (0-indexed >= 5): after 11, 5, 10 the middle anchor has
+    # nothing left and hands its turn to the last one (9).
+    assert on(pl.place_symmetric_bipolar(T, 4, 4, alpha=0.5)[0]) == [5, 9, 10, 11]
+    # The last anchor walks into the middle anchor's layers without taking one twice.
+    z, n, stop = pl.place_symmetric_bipolar(T, 4, 12)
+    assert on(z) == list(range(1, 12)) and n == 11 and stop == pl.STOP_NO_CONVERTIBLE
+    # P = 2: the middle stage is stage 0 (anchor 5); P = 1: one anchor.
+    assert on(pl.place_symmetric_bipolar([l // 6 for l in range(12)], 2, 2)[0]) == [5, 11]
+    assert [l for l, x in enumerate(pl.place_symmetric_bipolar([0] * 5, 1, 2)[0]) if x] == [3, 4]
+
+
+def test_placement_invariants_brute_force():
+    import random
+    rng = random.Random(5)
+    for _ in range(300):
+        P = rng.randint(1, 8)
+        N = rng.randint(2, 6)
+        Lr = P * N
+        stage = [l // N for l in range(Lr)]
+        # Equal stages, k <= P: one conversion in each of the last k stages.
+        k = rng.randint(0, P)
+        z, n, stop = pl.place_uniform(stage, P, k)
+        assert per_stage(stage, z, P) == [0] * (P - k) + [1] * k
+        # Symmetric, k small enough to stay inside the anchor stages: ceil(k/2) at the
+        # tail of the last stage, floor(k/2) at the tail of the middle stage.
+        if P >= 2:
+            mid = (P - 1) // 2
+            cap = N - 1 if mid == 0 else N
+            k2 = rng.randint(0, 2 * min(N, cap))
+            z, n, stop = pl.place_symmetric_bipolar(stage, P, k2)
+            c = per_stage(stage, z, P)
+            assert c[P - 1] == (k2 + 1) // 2 and c[mid] == k2 // 2 and sum(c) == k2
+            for i in (P - 1, mid):
+                got = [l for l in range(Lr) if z[l] and stage[l] == i]
+                end = max(l for l in range(Lr) if stage[l] == i)
+                assert got == list(range(end - len(got) + 1, end + 1))
+        # Any partition, mask and k: both place min(k, free layers), never layer 0,
+        # never an inadmissible layer.
+        cuts = sorted(rng.sample(range(1, Lr), P - 1)) if P > 1 else []
+        stage = [sum(1 for c in cuts if l >= c) for l in range(Lr)]
+        adm = [rng.random() < 0.7 for _ in range(Lr)]
+        k = rng.randint(0, Lr + 2)
+        free = sum(adm[1:])
+        for fn in (pl.place_uniform, pl.place_symmetric_bipolar):
+            z, n, stop = fn(stage, P, k, admissible=adm)
+            assert n == sum(z) == min(k, free) and z[0] == 0
+            assert all(adm[l] for l in range(Lr) if z[l])
+            assert stop == (pl.STOP_BUDGET if k <= free else pl.STOP_NO_CONVERTIBLE)
+
+
+def test_placement_rejects_bad_partitions():
+    with pytest.raises(ValueError):
+        pl.place_uniform([0, 1, 0], 2, 1)
+    with pytest.raises(ValueError):
+        pl.place_symmetric_bipolar([0, 2, 2], 3, 1)
+    with pytest.raises(ValueError):
+        pl.place_uniform([0, 0, 1], 2, -1)
+
+
 # ---------------------------------------------------------------------------
 # Hand-computed toys: stages {0,1,2},{3,4,5},{6,7,8},{9,10,11}, F(0) = 10, eps = 0.01.
 # ---------------------------------------------------------------------------
