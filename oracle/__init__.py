@@ -14,6 +14,9 @@ planner   -- App. A.7 FLOPs model, the FIR metric (Eqs. 4-5), stage FLOPs
              and the mask -> producer-map reading.
 attention -- Eq. (1)-(2) full attention, Eq. (3) cross-layer KV sharing, RoPE,
              the attention-only residual stack, and single-token decode.
+backward  -- the gradients of that stack (attention, RoPE, projections and
+             the residual), with a consumer's K/V gradient added to its
+             producer's.
 
 Every function is pinned by a test under ``tests/`` against values the paper
 prints, closed forms, invariants, library routines or brute force; the few
