@@ -75,6 +75,7 @@ extern "C" {
 
 #define KVP_PHASE_PREFILL   0
 #define KVP_PHASE_DECODE    1
+#define KVP_PHASE_BACKWARD  2  /* workspace of kvp_backward (kvp_workspace_size only) */
 
 #define KVP_STOP_FIR_MET        0  /* FIR <= 1 + eps                                    */
 #define KVP_STOP_BUDGET         1  /* m conversions made                                */
@@ -275,10 +276,13 @@ int kvp_set_kv_slot(kvp_ctx* ctx, int l, void* K, void* V);
 
 /*
  * kvp_workspace_size -- bytes of device scratch that a call with this phase,
- * batch B and length S (prefill; ignored for decode) needs.  The workspace
- * holds Q, the attention output, the fp32 residual stream and its bf16
- * copy, the RoPE table (prefill) and split-K partial results (decode).
- * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY (B > max_batch, S > max_seq).
+ * batch B and length S (prefill, backward; ignored for decode) needs.  The
+ * workspace holds Q, the attention output, the fp32 residual stream and its
+ * bf16 copy, the RoPE table (prefill) and split-K partial results (decode);
+ * for KVP_PHASE_BACKWARD (bf16 models) the gradients in flight, their
+ * transposed copies, transposed weights and the producers' fp32 dK/dV sums.
+ * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY (B > max_batch, S > max_seq),
+ * KVP_E_SHAPE (backward of an fp32 model).
  */
 int kvp_workspace_size(const kvp_ctx* ctx, int phase, int B, int S, size_t* bytes);
 
@@ -319,6 +323,62 @@ int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max
                     int B, void* ws, size_t ws_bytes, void* stream);
 
 /* ======================================================================== */
+/* Training: forward that keeps activations, and the backward pass           */
+/* ======================================================================== */
+/*
+ * Training a KV-shared model (the setting of Sec. 3) needs the gradients of the
+ * stack above.  bf16 models only (KVP_E_SHAPE for fp32).  The forward keeps, per
+ * layer l, in the caller's `saved` buffer: the post-RoPE Q_l and the attention
+ * output O_l ([B*S, a*d_h] bf16), the bf16 layer input X_l for l >= 1
+ * ([B*S, h]; X_0 is the caller's x), and the row log-sum-exp of the scaled
+ * scores ([B, a, Sp] fp32, log2 domain, Sp = S rounded up to 64).  The producers'
+ * K/V slots hold what the forward wrote; the backward reads them.
+ *
+ * The backward runs the layers last to first.  For layer l with producer
+ * p = tau(l): dW_O = G^T O_l and dO = G W_O with G = dLoss/dX_{l+1}; the
+ * attention gradients dQ, dK, dV (softmax Jacobian; dQ and dK rotated back
+ * through RoPE); a consumer adds its dK, dV to an fp32 buffer of its producer,
+ * and the producer adds that sum to its own (Eq. 3: K_p, V_p feed every layer
+ * that maps to p); then dW_Q = dQ^T X_l, for a producer dW_K = dK^T X_l and
+ * dW_V = dV^T X_l, and G += dQ W_Q (+ dK W_K + dV W_V).  Products on bf16
+ * matrix cores with fp32 accumulation; G is carried in fp32.
+ */
+
+/* kvp_train_saved_size -- bytes of the `saved` buffer for a call with B, S.
+ * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY, KVP_E_SHAPE (fp32 model). */
+int kvp_train_saved_size(const kvp_ctx* ctx, int B, int S, size_t* bytes);
+
+/*
+ * kvp_train_forward -- kvp_prefill that also fills `saved` (16-byte aligned,
+ * at least kvp_train_saved_size bytes).  Workspace: KVP_PHASE_PREFILL.
+ * Errors: as kvp_prefill, plus KVP_E_WORKSPACE for a short `saved` buffer and
+ * KVP_E_SHAPE for an fp32 model.
+ */
+int kvp_train_forward(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* saved,
+                      size_t saved_bytes, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kvp_set_layer_grads -- device buffers (fp32, caller-owned, 16-byte aligned)
+ * that kvp_backward overwrites with layer l's weight gradients, laid out like
+ * the weights: dWq [a*d_h, h], dWo [h, a*d_h]; dWk, dWv [g*d_h, h] for a
+ * producer, NULL for a consumer (it has no W_K, W_V).
+ * Errors: KVP_E_INVALID_ARG (l out of range, NULL / non-NULL mismatch).
+ */
+int kvp_set_layer_grads(kvp_ctx* ctx, int l, void* dWq, void* dWk, void* dWv, void* dWo);
+
+/*
+ * kvp_backward -- gradients of the last kvp_train_forward with the same x,
+ * B, S and saved buffer: dy = dLoss/dY [B*S, h] fp32 in, dx = dLoss/dX_0
+ * [B*S, h] fp32 out (dx must not alias dy or x), weight gradients into the
+ * buffers of kvp_set_layer_grads.  Workspace: KVP_PHASE_BACKWARD.
+ * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY, KVP_E_WORKSPACE, KVP_E_SHAPE,
+ * KVP_E_STATE (weights, slots or gradient buffers of some layer not set),
+ * KVP_E_HIP.
+ */
+int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* dx, int B, int S,
+                 const void* saved, size_t saved_bytes, void* ws, size_t ws_bytes, void* stream);
+
+/* ======================================================================== */
 /* Kernel timing (tracing)                                                    */
 /* ======================================================================== */
 
@@ -334,7 +394,11 @@ int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max
 #define KVP_K_DEC_OPROJ       8  /* decode: output projection + residual           */
 #define KVP_K_F32_ROPE        9  /* fp32 models: RoPE + scatter (prefill)          */
 #define KVP_K_F32_ATTN       10  /* fp32 models: attention                         */
-#define KVP_NUM_KERNEL_KINDS 11
+#define KVP_K_BWD_GEMM       11  /* backward: dO, weight-gradient and dX GEMMs      */
+#define KVP_K_BWD_ATTN_KV    12  /* backward: attention dK, dV                      */
+#define KVP_K_BWD_ATTN_Q     13  /* backward: attention dQ                          */
+#define KVP_K_BWD_AUX        14  /* backward: D, transposes, split-K sums, casts    */
+#define KVP_NUM_KERNEL_KINDS 15
 
 /*
  * kvp_profile_enable -- enable (1) or disable (0) kernel timing on ctx and

@@ -55,6 +55,7 @@ KIND_KCACHE = 6   # post-RoPE key cache contents, logical [B, g, pos, d_h]
 KIND_VCACHE = 7   # value cache contents, logical [B, g, pos, d_h]
 KIND_LENS = 8     # ragged decode context lengths [B]
 KIND_XDEC = 9     # decode input activations [B, h]
+KIND_DY = 10      # upstream gradient of the stack output [B, S, h] (always fp32)
 
 
 def _mix64_inplace(z: np.ndarray) -> np.ndarray:
@@ -323,6 +324,12 @@ def weight_shape(w: Workload, kind: int):
 def prefill_x(w: Workload, batch_ids: Sequence[int], positions: Sequence[int]) -> np.ndarray:
     idx = act_index(batch_ids, positions, w.h)
     return normal_values(w.seed, tensor_id(KIND_X), idx, w.x_sigma, w.dtype)
+
+
+def prefill_dy(w: Workload, batch_ids: Sequence[int], positions: Sequence[int]) -> np.ndarray:
+    """dLoss/dY rows (b, pos) -> [len(b), len(pos), h], fp32, standard normal."""
+    idx = act_index(batch_ids, positions, w.h)
+    return normal_values(w.seed, tensor_id(KIND_DY), idx, 1.0, "fp32")
 
 
 def decode_x(w: Workload, batch_ids: Sequence[int]) -> np.ndarray:

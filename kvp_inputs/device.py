@@ -13,7 +13,7 @@ import os
 
 import numpy as np
 
-from . import (KIND_KCACHE, KIND_VCACHE, KIND_WK, KIND_WO, KIND_WQ, KIND_WV, KIND_X, KIND_XDEC,
+from . import (KIND_DY, KIND_KCACHE, KIND_VCACHE, KIND_WK, KIND_WO, KIND_WQ, KIND_WV, KIND_X, KIND_XDEC,
                POS_STRIDE, Workload, normal_scale, stream_key, tensor_id, weight_shape)
 
 _LIB = None
@@ -58,6 +58,12 @@ def fill_weight(w: Workload, kind: int, layer: int, ptr: int, stream: int = 0) -
 def fill_prefill_x(w: Workload, ptr: int, B: int, S: int, stream: int = 0) -> None:
     """x [B, S, h] with the logical (b, pos, c) indexing of kvp_inputs.act_index."""
     fill(ptr, w.dtype, w.seed, tensor_id(KIND_X), w.x_sigma, [B, S, w.h],
+         [S * w.h, w.h, 1], [POS_STRIDE * w.h, w.h, 1], stream)
+
+
+def fill_prefill_dy(w: Workload, ptr: int, B: int, S: int, stream: int = 0) -> None:
+    """dLoss/dY [B, S, h] in fp32, indexed like the prefill input."""
+    fill(ptr, "fp32", w.seed, tensor_id(KIND_DY), 1.0, [B, S, w.h],
          [S * w.h, w.h, 1], [POS_STRIDE * w.h, w.h, 1], stream)
 
 

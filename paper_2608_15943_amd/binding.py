@@ -28,6 +28,7 @@ KVP_DTYPE_BF16 = 0
 KVP_DTYPE_FP32 = 1
 KVP_PHASE_PREFILL = 0
 KVP_PHASE_DECODE = 1
+KVP_PHASE_BACKWARD = 2
 KVP_STOP_FIR_MET = 0
 KVP_STOP_BUDGET = 1
 KVP_STOP_NO_CONVERTIBLE = 2
@@ -40,12 +41,14 @@ EXPORTS = [
     "kvp_create", "kvp_destroy", "kvp_set_layer", "kvp_set_kv_slot", "kvp_workspace_size",
     "kvp_prefill", "kvp_layer_forward", "kvp_decode_step", "kvp_get_map", "kvp_status_string",
     "kvp_last_error", "kvp_profile_enable", "kvp_profile_read",
+    "kvp_train_saved_size", "kvp_train_forward", "kvp_set_layer_grads", "kvp_backward",
     # include/kvp_calib.h: achievable-peak calibration (measurement support)
     "kvp_calib_mfma_bf16", "kvp_calib_stream_read",
 ]
 
 KERNEL_KINDS = ["rope_table", "qkv_gemm", "flash_attn", "oproj_gemm", "dec_gemm", "dec_rope",
-                "dec_attn", "dec_combine", "dec_oproj", "f32_rope", "f32_attn"]
+                "dec_attn", "dec_combine", "dec_oproj", "f32_rope", "f32_attn", "bwd_gemm",
+                "bwd_attn_kv", "bwd_attn_q", "bwd_aux"]
 
 
 class kvp_shape(C.Structure):
@@ -109,6 +112,10 @@ def lib() -> C.CDLL:
         "kvp_layer_forward": ([vp, i32, vp, vp, vp, i32, i32, vp, C.c_size_t, vp], i32),
         "kvp_decode_step": ([vp, vp, vp, i32, vp, i32, vp, C.c_size_t, vp], i32),
         "kvp_get_map": ([vp, C.POINTER(C.c_int32)], i32),
+        "kvp_train_saved_size": ([vp, i32, i32, C.POINTER(C.c_size_t)], i32),
+        "kvp_train_forward": ([vp, vp, vp, i32, i32, vp, C.c_size_t, vp, C.c_size_t, vp], i32),
+        "kvp_set_layer_grads": ([vp, i32, vp, vp, vp, vp], i32),
+        "kvp_backward": ([vp, vp, vp, vp, i32, i32, vp, C.c_size_t, vp, C.c_size_t, vp], i32),
         "kvp_status_string": ([i32], C.c_char_p),
         "kvp_last_error": ([], C.c_char_p),
         "kvp_profile_enable": ([vp, i32], i32),
@@ -257,6 +264,23 @@ class Model:
     def kvp_layer_forward(self, l, x, attn_out, y, B, S, ws, ws_bytes, stream=0):
         _check(lib().kvp_layer_forward(self.ctx, l, x, attn_out or None, y, B, S, ws, ws_bytes,
                                        stream or None), "kvp_layer_forward")
+
+    def kvp_train_saved_size(self, B, S) -> int:
+        n = C.c_size_t()
+        _check(lib().kvp_train_saved_size(self.ctx, B, S, C.byref(n)), "kvp_train_saved_size")
+        return n.value
+
+    def kvp_train_forward(self, x, y, B, S, saved, saved_bytes, ws, ws_bytes, stream=0):
+        _check(lib().kvp_train_forward(self.ctx, x, y, B, S, saved, saved_bytes, ws, ws_bytes,
+                                       stream or None), "kvp_train_forward")
+
+    def kvp_set_layer_grads(self, l, dwq, dwk, dwv, dwo):
+        _check(lib().kvp_set_layer_grads(self.ctx, l, dwq or None, dwk or None, dwv or None,
+                                         dwo or None), "kvp_set_layer_grads")
+
+    def kvp_backward(self, x, dy, dx, B, S, saved, saved_bytes, ws, ws_bytes, stream=0):
+        _check(lib().kvp_backward(self.ctx, x, dy, dx, B, S, saved, saved_bytes, ws, ws_bytes,
+                                  stream or None), "kvp_backward")
 
     def kvp_decode_step(self, x, len_dev, max_len, y, B, ws, ws_bytes, stream=0):
         _check(lib().kvp_decode_step(self.ctx, x, len_dev, max_len, y, B, ws, ws_bytes,

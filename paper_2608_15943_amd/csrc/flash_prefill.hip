@@ -1,5 +1,7 @@
 // Causal flash attention for the prefill / training forward (Sec. 2.2, Eq. 2),
-// bf16 matrix cores, d_h = 128, GQA: query head j reads KV head j / r.
+// bf16 matrix cores, d_h = 128, GQA: query head j reads KV head j / r.  For training
+// it also stores each query's log-sum-exp of the scaled scores (log2 domain), from
+// which the backward rebuilds the softmax weights.
 //
 // A consumer layer runs the same kernel on its producer's slot (Eq. 3); the
 // kernel only sees a K slot and a V slot.
@@ -65,7 +67,8 @@ __device__ __forceinline__ int swap_b23(int r) { return (r & ~12) | ((r & 4) << 
 // 8 waves of 32 queries; two waves per SIMD (<= 256 registers each), 128 KB of LDS.
 __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
-    uint16_t* __restrict__ O, int B, int S, int a, int g, int cap, float scale_log2) {
+    uint16_t* __restrict__ O, float* __restrict__ lse, int Sp, int B, int S, int a, int g, int cap,
+    float scale_log2) {
     // K: [stage][row * 16 + (chunk ^ (row & 15))]; V^T: [stage][d * 16 + (chunk ^ (d & 15))]
     // (rows of 256 bytes: 128 dims of a position, or 128 positions of a dim).
     __shared__ u32x4 lk[2][BKV * 16];
@@ -275,6 +278,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     if (q_lane < S) {
         const float l_tot = pair32_sum(l_run);
         const float inv = 1.0f / l_tot;
+        if (lse && hi == 0) lse[((size_t)b * a + head) * Sp + q_lane] = m_run + log2f(l_tot);
         uint16_t* orow = O + ((size_t)b * S + q_lane) * ldq + head * D;
 #pragma unroll
         for (int db = 0; db < 4; ++db)
@@ -292,11 +296,12 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
 }  // namespace
 
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                              uint16_t* o, int B, int S, int a, int g, int cap, hipStream_t st) {
+                              uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
+                              hipStream_t st) {
     const int nqt = (S + BQ - 1) / BQ;
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-    hipLaunchKernelGGL(flash_prefill_kernel, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, B, S,
-                       a, g, cap, scale_log2);
+    hipLaunchKernelGGL(flash_prefill_kernel, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, lse, Sp,
+                       B, S, a, g, cap, scale_log2);
     return hipGetLastError();
 }
 

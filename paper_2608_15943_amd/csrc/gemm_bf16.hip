@@ -66,6 +66,7 @@ struct QkvEpi {
         u32x4 cs[8][4];
     };
     QkvOut o;
+    __device__ __forceinline__ void set_split(int) {}
     // Region of the wave's 128 columns: 0 = Q, 1 = K, 2 = V, -1 = past N.
     __device__ __forceinline__ int region(int nw, int N, int* head) const {
         if (nw >= N) return -1;
@@ -213,6 +214,7 @@ struct ResidEpi {
     const void* x;
     uint16_t* y;
     float* yf;
+    __device__ __forceinline__ void set_split(int) {}
     __device__ __forceinline__ void stage(int pass, f32x16 (&acc)[4][4], int mw, int nw, int lane,
                                           int M, int N, char* st) const {
         if (nw >= N) return;
@@ -283,6 +285,56 @@ struct ResidEpi {
     }
 };
 
+// Plain store of C (no fused work): bf16 [M][N], or fp32 partial sums of one K slice into
+// plane `split` of out ([M][N] per plane).  Staged like ResidEpi, two passes of 64 columns.
+struct OutEpi {
+    static constexpr int kPasses = 2;
+    struct Pre {};
+    void* out;
+    size_t plane;
+    int split;
+    bool bf16;
+    __device__ __forceinline__ void set_split(int s) { split = s; }
+    __device__ __forceinline__ void stage(int pass, f32x16 (&acc)[4][4], int mw, int nw, int lane,
+                                          int M, int N, char* st) const {
+        if (nw >= N) return;
+        const int l32 = lane & 31, hi = lane >> 5;
+#pragma unroll
+        for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+            for (int i = 0; i < 16; ++i) {
+                const int m = 32 * mb + 8 * (i >> 2) + 4 * hi + (i & 3);
+                st_f32(st, m, l32, pass == 0 ? acc[mb][0][i] : acc[mb][2][i]);
+                st_f32(st, m, 32 + l32, pass == 0 ? acc[mb][1][i] : acc[mb][3][i]);
+            }
+    }
+    __device__ __forceinline__ void prefetch(int, int, int, int, int, int, Pre&) const {}
+    __device__ __forceinline__ void flush(int pass, int mw, int nw, int lane, int M, int N,
+                                          const char* st, const Pre&) const {
+        if (nw >= N) return;
+#pragma unroll
+        for (int it = 0; it < 16; ++it) {
+            const int ml = 8 * it + (lane >> 3), c8 = lane & 7;
+            const int m = mw + ml;
+            if (m >= M) continue;
+            const u32x4 p0 = ld_f32(st, ml, 2 * c8), p1 = ld_f32(st, ml, 2 * c8 + 1);
+            const size_t off = (size_t)m * N + nw + 64 * pass + 8 * c8;
+            if (bf16) {
+                u32x4 o;
+                o[0] = pack2bf(__uint_as_float(p0[0]), __uint_as_float(p0[1]));
+                o[1] = pack2bf(__uint_as_float(p0[2]), __uint_as_float(p0[3]));
+                o[2] = pack2bf(__uint_as_float(p1[0]), __uint_as_float(p1[1]));
+                o[3] = pack2bf(__uint_as_float(p1[2]), __uint_as_float(p1[3]));
+                *(u32x4*)((uint16_t*)out + off) = o;
+            } else {
+                float* dst = (float*)out + split * plane + off;
+                *(u32x4*)dst = p0;
+                *(u32x4*)(dst + 4) = p1;
+            }
+        }
+    }
+};
+
 typedef __attribute__((address_space(1))) void gvoid_t;
 typedef __attribute__((address_space(3))) void lvoid_t;
 
@@ -292,14 +344,20 @@ __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
 template <class Epi>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict__ A, WRows W,
-                                                     int M, int N, int K, Epi epi) {
+                                                     int M, int N, int K, int splits, Epi epi) {
     __shared__ u32x4 lds[2][2][BM * 8];  // [stage][A, W][row * 8 + swizzled chunk]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave >> 1, wn = wave & 1;
 
     const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN;
-    const int lid = xcd_remap(blockIdx.x, gridDim.x);
+    // With split K, workgroup slot `split` of every tile takes K columns
+    // [split * K / splits, (split + 1) * K / splits); consecutive ids share a slice.
+    const int lid0 = xcd_remap(blockIdx.x, gridDim.x);
+    const int split = lid0 / (ntm * ntn);
+    const int lid = lid0 - split * (ntm * ntn);
+    const int kofs = split * (K / splits);
+    epi.set_split(split);
     const int group = lid / (GROUP_M * ntn), first = group * GROUP_M;
     const int gsz = min(ntm - first, GROUP_M);
     const int in_g = lid - group * GROUP_M * ntn;
@@ -314,8 +372,8 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
     for (int j = 0; j < 8; ++j) {
         const int row = 64 * wave + 8 * j + (lane >> 3);
         const int c = swz(row, lane & 7);
-        a_src[j] = A + (size_t)min(m0 + row, M - 1) * K + 8 * c;
-        w_src[j] = w_row(W, min(n0 + row, N - 1), K) + 8 * c;
+        a_src[j] = A + (size_t)min(m0 + row, M - 1) * K + kofs + 8 * c;
+        w_src[j] = w_row(W, min(n0 + row, N - 1), K) + kofs + 8 * c;
     }
     // Row group j (8 rows of A and of W) of tile kt into stage stg.
     auto issue_part = [&](int kt, int stg, int j) {
@@ -336,7 +394,7 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
 #pragma unroll
         for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
 
-    const int nk = K / BK;
+    const int nk = K / splits / BK;
     const int l32 = lane & 31, hi = lane >> 5;
     int a_off[4], b_off[4], rsw[4], bsw[4];
 #pragma unroll
@@ -420,9 +478,10 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
 
 template <class Epi>
 hipError_t launch(const uint16_t* A, const WRows& W, int M, int N, int K, const Epi& epi,
-                  hipStream_t st) {
+                  hipStream_t st, int splits = 1) {
     const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    hipLaunchKernelGGL(gemm_bf16_nt<Epi>, dim3(tiles), dim3(NT), 0, st, A, W, M, N, K, epi);
+    hipLaunchKernelGGL(gemm_bf16_nt<Epi>, dim3(tiles * splits), dim3(NT), 0, st, A, W, M, N, K, splits,
+                       epi);
     return hipGetLastError();
 }
 
@@ -438,6 +497,22 @@ hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_r
     WRows W{{w, nullptr, nullptr}, {N, 0, 0}};
     if (x_f32) return launch(a, W, M, N, K, ResidEpi<true>{x_res, y, yf}, st);
     return launch(a, W, M, N, K, ResidEpi<false>{x_res, y, yf}, st);
+}
+
+int gemm_out_splits(int M, int N, int K) {
+    const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    const int nk = K / BK;
+    int s = 1;
+    // One workgroup per CU: split K until the grid covers the 256 CUs (at most 8 slices).
+    while (tiles * s < 256 && s < 8 && nk % (2 * s) == 0) s *= 2;
+    return s;
+}
+
+hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits,
+                         void* part, bool bf16_out, hipStream_t st) {
+    WRows W{{w, nullptr, nullptr}, {N, 0, 0}};
+    if (splits < 1 || (K / BK) % splits || (bf16_out && splits != 1)) return hipErrorInvalidValue;
+    return launch(a, W, M, N, K, OutEpi{part, (size_t)M * N, 0, bf16_out}, st, splits);
 }
 
 }  // namespace kvp

@@ -34,9 +34,71 @@ hipError_t gemm_qkv_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
 hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_res, bool x_f32,
                            uint16_t* y, float* yf, int M, int N, int K, hipStream_t st);
 
-// Causal flash attention: q [B*S][a*128], K/V slots of the producer, o [B*S][a*128].
+// Causal flash attention: q [B*S][a*128], K/V slots of the producer, o [B*S][a*128];
+// lse (optional) [B][a][Sp]: the row log-sum-exp of the scaled scores, log2 domain.
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                              uint16_t* o, int B, int S, int a, int g, int cap, hipStream_t st);
+                              uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
+                              hipStream_t st);
+
+// C = A @ W^T (A [M][K], W [N][K], K % 64 == 0) split over `splits` equal slices of K:
+// slice s writes its fp32 partial sum to part + s * M * N ([M][N] each), or, with
+// bf16_out, a single slice writes bf16 C [M][N] to part.
+hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits,
+                         void* part, bool bf16_out, hipStream_t st);
+// The slice count gemm_out_bf16 should use for an M x N x K product on this device.
+int gemm_out_splits(int M, int N, int K);
+
+// ---- bf16 backward ----------------------------------------------------------
+
+// out[p][c][r] = in[p][r][c] (r < R, c < C), zero for R <= r < Rp, C <= c < Cp.
+hipError_t transpose_bf16(const uint16_t* in, uint16_t* out, int planes, int R, int C, size_t in_ld,
+                          size_t in_plane, size_t out_ld, size_t out_plane, int Rp, int Cp,
+                          hipStream_t st);
+hipError_t f32_to_bf16(const float* x, uint16_t* y, size_t n, hipStream_t st);
+// Sum of `planes` [M][N] fp32 planes; rows [0, rows0) -> dst0, then rows1 -> dst1, rest -> dst2.
+hipError_t reduce_planes(const float* part, int planes, int M, int N, float* dst0, int rows0, float* dst1,
+                         int rows1, float* dst2, hipStream_t st);
+// D = rowsum(dO * O) [B][a][Sp] and dO^T, Q^T, O^T [a*128][B*Sp] (zero past S).
+hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, const uint16_t* Q, float* dsum,
+                              uint16_t* dOt, uint16_t* Qt, uint16_t* Ot, int B, int S, int Sp, int a,
+                              hipStream_t st);
+
+struct AttnBwdKv {
+    const uint16_t* q;
+    const uint16_t* qt;
+    const uint16_t* dO;
+    const uint16_t* dOt;
+    const float* lse;
+    const float* dsum;
+    const uint16_t* kc;
+    const uint16_t* vc;
+    const float2* rope;
+    const float* acc_in_k;
+    const float* acc_in_v;
+    float* acc_out_k;
+    float* acc_out_v;
+    uint16_t* out;
+    uint16_t* outT;
+    int ldo, col_k, col_v;
+    int B, S, Sp, a, g, cap;
+};
+hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st);
+
+struct AttnBwdQ {
+    const uint16_t* q;
+    const uint16_t* dO;
+    const float* lse;
+    const float* dsum;
+    const uint16_t* kc;
+    const uint16_t* kt;
+    const uint16_t* vr;
+    const float2* rope;
+    uint16_t* out;
+    uint16_t* outT;
+    int ldo;
+    int B, S, Sp, a, g, cap;
+};
+hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st);
 
 // ---- bf16 decode ------------------------------------------------------------
 // Largest decode grid (waves); the combine keeps one weight per wave of a pair in LDS.

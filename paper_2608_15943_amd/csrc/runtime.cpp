@@ -41,6 +41,11 @@ struct Layer {
     void* kc = nullptr;
     void* vc = nullptr;
     bool weights = false;
+    float* dwq = nullptr;   // weight gradients (training), fp32
+    float* dwk = nullptr;
+    float* dwv = nullptr;
+    float* dwo = nullptr;
+    bool grads = false;
 };
 
 constexpr size_t kAlign = 256;
@@ -209,7 +214,8 @@ kvp::WRows proj_rows(const kvp_ctx* c, int l, bool producer) {
 // One prefill layer over rows [B*S]: io.a -> projections, io.res + O W_O^T -> io.y
 // (and io.yf), attention output into o_buf.
 int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* ws,
-                      const Workspace& w, int B, int S, hipStream_t st) {
+                      const Workspace& w, int B, int S, hipStream_t st, void* q_buf = nullptr,
+                      float* lse = nullptr) {
     const int p = c->tau[l];
     const bool producer = p == l;
     const Layer& P = c->layers[p];
@@ -222,7 +228,7 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
     int rc;
     if (c->bf16()) {
         kvp::QkvOut qo{};
-        qo.q = (uint16_t*)(ws + w.q);
+        qo.q = (uint16_t*)(q_buf ? q_buf : ws + w.q);
         qo.kc = producer ? (uint16_t*)P.kc : nullptr;
         qo.vc = producer ? (uint16_t*)P.vc : nullptr;
         qo.rope = (const float2*)(ws + w.rope);
@@ -238,8 +244,9 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
             return rc;
         if ((rc = timed(c, KVP_K_FLASH_ATTN, st, [&] {
                  return check_hip(kvp::flash_prefill_bf16(qo.q, (const uint16_t*)P.kc,
-                                                          (const uint16_t*)P.vc, (uint16_t*)o_buf, B,
-                                                          S, c->d.a, c->d.g, c->d.kv_capacity, st),
+                                                          (const uint16_t*)P.vc, (uint16_t*)o_buf, lse,
+                                                          (S + 63) / 64 * 64, B, S, c->d.a, c->d.g,
+                                                          c->d.kv_capacity, st),
                                   "flash attention");
              })))
             return rc;
@@ -504,15 +511,106 @@ extern "C" int kvp_set_kv_slot(kvp_ctx* ctx, int l, void* K, void* V) {
     return ok();
 }
 
+namespace {
+
+// ---- training --------------------------------------------------------------
+
+int round64(int S) { return (S + 63) / 64 * 64; }
+
+// Per-layer activations of kvp_train_forward, layer l at l * stride.
+struct Saved {
+    size_t q = 0, o = 0, x = 0, lse = 0, stride = 0, total = 0;
+};
+
+Saved saved_layout(const kvp_ctx& c, int B, int S) {
+    Saved v;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align_up(bytes);
+        return at;
+    };
+    const size_t M = (size_t)B * S;
+    v.q = take(M * c.n_q() * 2);
+    v.o = take(M * c.n_q() * 2);
+    v.x = take(M * c.d.h * 2);
+    v.lse = take((size_t)B * c.d.a * round64(S) * sizeof(float));
+    v.stride = off;
+    v.total = off * c.d.L;
+    return v;
+}
+
+// Workspace of kvp_backward.
+struct BwdWs {
+    size_t gb = 0, gbt = 0, dO = 0, dOt = 0, qt = 0, ot = 0, xt = 0, dsum = 0, dqkv = 0, dqkvt = 0;
+    size_t kt = 0, vr = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
+    size_t acc_plane = 0;          // floats of one dK or dV sum
+    std::vector<int> acc_slot;     // per layer: index of its fp32 sum pair, or -1
+};
+
+BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
+    BwdWs w;
+    size_t off = 0;
+    auto take = [&](size_t bytes) {
+        const size_t at = off;
+        off += align_up(bytes);
+        return at;
+    };
+    const size_t M = (size_t)B * S, Sp = round64(S), T = (size_t)B * Sp;
+    const size_t h = c.d.h, nq = c.n_q(), nkv = c.n_kv(), np = nq + 2 * nkv;
+    w.gb = take(M * h * 2);
+    w.gbt = take(h * T * 2);
+    w.dO = take(M * nq * 2);
+    w.dOt = take(nq * T * 2);
+    w.qt = take(nq * T * 2);
+    w.ot = take(nq * T * 2);
+    w.xt = take(h * T * 2);
+    w.dsum = take((size_t)B * c.d.a * Sp * sizeof(float));
+    w.dqkv = take(M * np * 2);
+    w.dqkvt = take(np * T * 2);
+    w.kt = take((size_t)B * c.d.g * 128 * Sp * 2);
+    w.vr = take((size_t)B * c.d.g * Sp * 128 * 2);
+    // One fp32 dK/dV pair per producer that has consumers.
+    w.acc_slot.assign(c.d.L, -1);
+    int nacc = 0;
+    for (int l = 0; l < c.d.L; ++l)
+        if (c.tau[l] == l)
+            for (int j = l + 1; j < c.d.L; ++j)
+                if (c.tau[j] == l) {
+                    w.acc_slot[l] = nacc++;
+                    break;
+                }
+    w.acc_plane = (size_t)B * c.d.g * S * 128;
+    w.acc = take((size_t)nacc * 2 * w.acc_plane * sizeof(float));
+    w.wot = take(nq * h * 2);
+    w.wst = take(h * np * 2);
+    // Split-K partial planes of the weight-gradient GEMMs (consumers: Q rows only).
+    const int so = kvp::gemm_out_splits((int)h, (int)nq, (int)T);
+    const int sp = kvp::gemm_out_splits((int)np, (int)h, (int)T);
+    const int sc = kvp::gemm_out_splits((int)nq, (int)h, (int)T);
+    w.part = take(std::max({(size_t)so * h * nq, (size_t)sp * np * h, (size_t)sc * nq * h}) * sizeof(float));
+    w.rope = take((size_t)S * 64 * sizeof(float2));
+    w.total = off;
+    return w;
+}
+
+}  // namespace
+
 extern "C" int kvp_workspace_size(const kvp_ctx* ctx, int phase, int B, int S, size_t* bytes) {
     if (!ctx || !bytes) return fail(KVP_E_INVALID_ARG, "kvp_workspace_size: NULL argument");
-    if (phase != KVP_PHASE_PREFILL && phase != KVP_PHASE_DECODE)
+    if (phase != KVP_PHASE_PREFILL && phase != KVP_PHASE_DECODE && phase != KVP_PHASE_BACKWARD)
         return fail(KVP_E_INVALID_ARG, "kvp_workspace_size: unknown phase");
-    if (B < 1 || (phase == KVP_PHASE_PREFILL && S < 1))
+    const bool seq = phase != KVP_PHASE_DECODE;
+    if (B < 1 || (seq && S < 1))
         return fail(KVP_E_INVALID_ARG, "kvp_workspace_size: B and S must be >= 1");
     if (B > ctx->d.max_batch) return fail(KVP_E_CAPACITY, "kvp_workspace_size: B > max_batch");
-    if (phase == KVP_PHASE_PREFILL && S > ctx->d.max_seq)
+    if (seq && S > ctx->d.max_seq)
         return fail(KVP_E_CAPACITY, "kvp_workspace_size: S > max_seq");
+    if (phase == KVP_PHASE_BACKWARD) {
+        if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_workspace_size: the backward needs a bf16 model");
+        *bytes = bwd_layout(*ctx, B, S).total;
+        return ok();
+    }
     *bytes = layout(*ctx, phase, B, phase == KVP_PHASE_PREFILL ? S : 1).total;
     return ok();
 }
@@ -606,6 +704,265 @@ extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_d
     for (int l = 0; l < L; ++l) {
         const LayerIO io = stack_io(ctx->bf16(), l, L, x, y, base, w);
         if ((rc = run_decode_layer(ctx, l, io, len_dev, max_len, base, w, B, st))) return rc;
+    }
+    return ok();
+}
+
+// ============================================================================
+// Training
+// ============================================================================
+
+extern "C" int kvp_train_saved_size(const kvp_ctx* ctx, int B, int S, size_t* bytes) {
+    if (!ctx || !bytes) return fail(KVP_E_INVALID_ARG, "kvp_train_saved_size: NULL argument");
+    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_train_saved_size: training needs a bf16 model");
+    if (B < 1 || S < 1) return fail(KVP_E_INVALID_ARG, "kvp_train_saved_size: B and S must be >= 1");
+    if (B > ctx->d.max_batch || S > ctx->d.max_seq)
+        return fail(KVP_E_CAPACITY, "kvp_train_saved_size: B or S beyond max_batch / max_seq");
+    *bytes = saved_layout(*ctx, B, S).total;
+    return ok();
+}
+
+extern "C" int kvp_train_forward(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* saved,
+                                 size_t saved_bytes, void* ws, size_t ws_bytes, void* stream) {
+    Workspace w;
+    int rc = check_prefill_args(ctx, x, y, B, S, ws, ws_bytes, &w);
+    if (rc) return rc;
+    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_train_forward: training needs a bf16 model");
+    const Saved sv = saved_layout(*ctx, B, S);
+    if (!saved || saved_bytes < sv.total || !aligned16(saved))
+        return fail(KVP_E_WORKSPACE, "kvp_train_forward: saved buffer needs %zu bytes (16-byte aligned), got %zu",
+                    sv.total, saved ? saved_bytes : (size_t)0);
+    if ((rc = check_layers(ctx, 0, ctx->d.L))) return rc;
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)ws;
+    char* sb = (char*)saved;
+    if ((rc = timed(ctx, KVP_K_ROPE_TABLE, st, [&] {
+             return check_hip(kvp::rope_table((float2*)(base + w.rope), S, ctx->d.d_h, ctx->d.rope_base, st),
+                              "RoPE table");
+         })))
+        return rc;
+    const int L = ctx->d.L;
+    float* xr = (float*)(base + w.xr);
+    for (int l = 0; l < L; ++l) {
+        char* lay = sb + (size_t)l * sv.stride;
+        LayerIO io;
+        io.a = l == 0 ? x : (const void*)(lay + sv.x);
+        io.res = l == 0 ? x : (const void*)xr;
+        io.res_f32 = l != 0;
+        io.y = l == L - 1 ? y : (void*)(sb + (size_t)(l + 1) * sv.stride + sv.x);
+        io.yf = l == L - 1 ? nullptr : xr;
+        if ((rc = run_prefill_layer(ctx, l, io, lay + sv.o, base, w, B, S, st, lay + sv.q,
+                                    (float*)(lay + sv.lse))))
+            return rc;
+    }
+    return ok();
+}
+
+extern "C" int kvp_set_layer_grads(kvp_ctx* ctx, int l, void* dWq, void* dWk, void* dWv, void* dWo) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "kvp_set_layer_grads: NULL ctx");
+    if (l < 0 || l >= ctx->d.L) return fail(KVP_E_INVALID_ARG, "kvp_set_layer_grads: layer %d out of range", l);
+    const bool producer = ctx->tau[l] == l;
+    if (!dWq || !dWo) return fail(KVP_E_INVALID_ARG, "kvp_set_layer_grads: dWq and dWo are required");
+    if (producer && (!dWk || !dWv))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_layer_grads: layer %d is a producer and needs dWk, dWv", l);
+    if (!producer && (dWk || dWv))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_layer_grads: layer %d has no W_K, W_V", l);
+    if (!aligned16(dWq) || !aligned16(dWo) || (dWk && !aligned16(dWk)) || (dWv && !aligned16(dWv)))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_layer_grads: buffers must be 16-byte aligned");
+    Layer& L = ctx->layers[l];
+    L.dwq = (float*)dWq;
+    L.dwk = (float*)dWk;
+    L.dwv = (float*)dWv;
+    L.dwo = (float*)dWo;
+    L.grads = true;
+    return ok();
+}
+
+extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* dx, int B, int S,
+                            const void* saved, size_t saved_bytes, void* ws, size_t ws_bytes,
+                            void* stream) {
+    if (!ctx || !x || !dy || !dx) return fail(KVP_E_INVALID_ARG, "kvp_backward: NULL argument");
+    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_backward: training needs a bf16 model");
+    if (dx == dy || dx == x) return fail(KVP_E_INVALID_ARG, "kvp_backward: dx must not alias dy or x");
+    if (!aligned16(x) || !aligned16(dy) || !aligned16(dx))
+        return fail(KVP_E_INVALID_ARG, "kvp_backward: x, dy, dx must be 16-byte aligned");
+    if (B < 1 || S < 1) return fail(KVP_E_INVALID_ARG, "kvp_backward: B and S must be >= 1");
+    if (B > ctx->d.max_batch || S > ctx->d.max_seq)
+        return fail(KVP_E_CAPACITY, "kvp_backward: B=%d, S=%d exceed max_batch / max_seq", B, S);
+    const int h = ctx->d.h, nq = ctx->n_q(), nkv = ctx->n_kv(), L = ctx->d.L;
+    const int Sp = round64(S), M = B * S, T = B * Sp;
+    if ((int64_t)(nq + 2 * nkv) * T > INT32_MAX || (int64_t)M * std::max(h, nq + 2 * nkv) > INT32_MAX)
+        return fail(KVP_E_SHAPE, "kvp_backward: sizes exceed the 32-bit index range");
+    const Saved sv = saved_layout(*ctx, B, S);
+    if (!saved || saved_bytes < sv.total || !aligned16(saved))
+        return fail(KVP_E_WORKSPACE, "kvp_backward: saved buffer needs %zu bytes, got %zu", sv.total,
+                    saved ? saved_bytes : (size_t)0);
+    const BwdWs w = bwd_layout(*ctx, B, S);
+    if (!ws || ws_bytes < w.total || !aligned16(ws))
+        return fail(KVP_E_WORKSPACE, "kvp_backward: workspace needs %zu bytes (16-byte aligned), got %zu",
+                    w.total, ws ? ws_bytes : (size_t)0);
+    int rc;
+    if ((rc = check_layers(ctx, 0, L))) return rc;
+    for (int l = 0; l < L; ++l)
+        if (!ctx->layers[l].grads)
+            return fail(KVP_E_STATE, "kvp_backward: gradient buffers of layer %d were never set", l);
+
+    hipStream_t st = (hipStream_t)stream;
+    char* base = (char*)ws;
+    const char* sb = (const char*)saved;
+    auto bp = [&](size_t off) { return (uint16_t*)(base + off); };
+    uint16_t *gb = bp(w.gb), *gbt = bp(w.gbt), *dO = bp(w.dO), *dOt = bp(w.dOt), *qt = bp(w.qt),
+             *ot = bp(w.ot), *xt = bp(w.xt), *dqkv = bp(w.dqkv), *dqkvt = bp(w.dqkvt), *kt = bp(w.kt),
+             *vr = bp(w.vr), *wot = bp(w.wot), *wst = bp(w.wst);
+    float* dsum = (float*)(base + w.dsum);
+    float* acc = (float*)(base + w.acc);
+    float* part = (float*)(base + w.part);
+    const float2* rope = (const float2*)(base + w.rope);
+    const size_t tld = (size_t)T;
+    auto aux = [&](auto&& f) { return timed(ctx, KVP_K_BWD_AUX, st, f); };
+    auto gemm = [&](auto&& f) { return timed(ctx, KVP_K_BWD_GEMM, st, f); };
+
+    if ((rc = aux([&] {
+             return check_hip(kvp::rope_table((float2*)rope, S, 128, ctx->d.rope_base, st), "RoPE table");
+         })))
+        return rc;
+    if ((rc = aux([&] { return check_hip(kvp::f32_to_bf16((const float*)dy, gb, (size_t)M * h, st), "cast dY"); })))
+        return rc;
+
+    std::vector<char> acc_written(L, 0);
+    int kt_owner = -1;
+    for (int l = L - 1; l >= 0; --l) {
+        const int p = ctx->tau[l];
+        const bool producer = p == l;
+        const int np = producer ? nq + 2 * nkv : nq;
+        const Layer& Ly = ctx->layers[l];
+        const Layer& Pl = ctx->layers[p];
+        const char* lay = sb + (size_t)l * sv.stride;
+        const uint16_t* Ql = (const uint16_t*)(lay + sv.q);
+        const uint16_t* Ol = (const uint16_t*)(lay + sv.o);
+        const float* lse = (const float*)(lay + sv.lse);
+        const uint16_t* Xl = l == 0 ? (const uint16_t*)x : (const uint16_t*)(lay + sv.x);
+
+        // dO = G W_O (W_O^T as the [a*d_h][h] operand), then D and the transposed copies.
+        if ((rc = aux([&] {
+                 return check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wo, wot, 1, h, nq, nq, 0, h, 0, h, nq, st),
+                                  "transpose W_O");
+             })))
+            return rc;
+        if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gb, wot, M, nq, h, 1, dO, true, st), "dO GEMM"); })))
+            return rc;
+        if ((rc = aux([&] {
+                 return check_hip(kvp::attn_bwd_prep_bf16(dO, Ol, Ql, dsum, dOt, qt, ot, B, S, Sp, ctx->d.a, st),
+                                  "attention backward prep");
+             })))
+            return rc;
+        // dW_O = G^T O.
+        if ((rc = aux([&] {
+                 return check_hip(kvp::transpose_bf16(gb, gbt, B, S, h, h, (size_t)S * h, tld, Sp, Sp, h, st),
+                                  "transpose G");
+             })))
+            return rc;
+        {
+            const int s = kvp::gemm_out_splits(h, nq, T);
+            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gbt, ot, h, nq, T, s, part, false, st), "dW_O GEMM"); })))
+                return rc;
+            if ((rc = aux([&] {
+                     return check_hip(kvp::reduce_planes(part, s, h, nq, Ly.dwo, h, nullptr, 0, nullptr, st), "dW_O sum");
+                 })))
+                return rc;
+        }
+        // The producer's K^T and V rows for the dQ kernel.
+        if (kt_owner != p) {
+            const int planes = B * ctx->d.g, cap = ctx->d.kv_capacity;
+            if ((rc = aux([&] {
+                     int r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Pl.kc, kt, planes, S, 128, 128,
+                                                            (size_t)cap * 128, Sp, (size_t)128 * Sp, Sp, 128, st),
+                                        "transpose K");
+                     if (!r2)
+                         r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Pl.vc, vr, planes, 128, S, cap,
+                                                            (size_t)128 * cap, 128, (size_t)Sp * 128, 128, Sp, st),
+                                        "transpose V");
+                     return r2;
+                 })))
+                return rc;
+            kt_owner = p;
+        }
+        // dK, dV: a consumer adds into its producer's fp32 sums; the producer finishes them.
+        {
+            kvp::AttnBwdKv a{};
+            a.q = Ql; a.qt = qt; a.dO = dO; a.dOt = dOt; a.lse = lse; a.dsum = dsum;
+            a.kc = (const uint16_t*)Pl.kc; a.vc = (const uint16_t*)Pl.vc; a.rope = rope;
+            const int slot = w.acc_slot[p];
+            float* ak = slot >= 0 ? acc + (size_t)slot * 2 * w.acc_plane : nullptr;
+            float* av = slot >= 0 ? ak + w.acc_plane : nullptr;
+            if (!producer) {
+                a.acc_in_k = acc_written[p] ? ak : nullptr;
+                a.acc_in_v = acc_written[p] ? av : nullptr;
+                a.acc_out_k = ak;
+                a.acc_out_v = av;
+                acc_written[p] = 1;
+            } else {
+                a.acc_in_k = acc_written[l] ? ak : nullptr;
+                a.acc_in_v = acc_written[l] ? av : nullptr;
+                a.out = dqkv;
+                a.outT = dqkvt;
+                a.ldo = np;
+                a.col_k = nq;
+                a.col_v = nq + nkv;
+            }
+            a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
+            if ((rc = timed(ctx, KVP_K_BWD_ATTN_KV, st, [&] {
+                     return check_hip(kvp::flash_bwd_kv_bf16(a, st), "attention backward dK dV");
+                 })))
+                return rc;
+        }
+        {
+            kvp::AttnBwdQ a{};
+            a.q = Ql; a.dO = dO; a.lse = lse; a.dsum = dsum; a.kc = (const uint16_t*)Pl.kc; a.kt = kt;
+            a.vr = vr; a.rope = rope; a.out = dqkv; a.outT = dqkvt; a.ldo = np;
+            a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
+            if ((rc = timed(ctx, KVP_K_BWD_ATTN_Q, st, [&] {
+                     return check_hip(kvp::flash_bwd_q_bf16(a, st), "attention backward dQ");
+                 })))
+                return rc;
+        }
+        // dW_Q (| dW_K | dW_V) = [dQ | dK | dV]^T X_l.
+        if ((rc = aux([&] {
+                 return check_hip(kvp::transpose_bf16(Xl, xt, B, S, h, h, (size_t)S * h, tld, Sp, Sp, h, st),
+                                  "transpose X");
+             })))
+            return rc;
+        {
+            const int s = kvp::gemm_out_splits(np, h, T);
+            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(dqkvt, xt, np, h, T, s, part, false, st), "dW_QKV GEMM"); })))
+                return rc;
+            if ((rc = aux([&] {
+                     return check_hip(kvp::reduce_planes(part, s, np, h, Ly.dwq, nq, Ly.dwk, producer ? nkv : 0,
+                                                         Ly.dwv, st),
+                                      "dW_QKV sum");
+                 })))
+                return rc;
+        }
+        // G += [dQ | dK | dV] [W_Q; W_K; W_V] (the stacked weights transposed to [h][np]).
+        if ((rc = aux([&] {
+                 int r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wq, wst, 1, nq, h, h, 0, np, 0, nq, h, st),
+                                    "transpose W_Q");
+                 if (!r2 && producer)
+                     r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wk, wst + nq, 1, nkv, h, h, 0, np, 0, nkv,
+                                                        h, st),
+                                    "transpose W_K");
+                 if (!r2 && producer)
+                     r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wv, wst + nq + nkv, 1, nkv, h, h, 0, np, 0,
+                                                        nkv, h, st),
+                                    "transpose W_V");
+                 return r2;
+             })))
+            return rc;
+        const void* gres = l == L - 1 ? dy : dx;
+        if ((rc = gemm([&] {
+                 return check_hip(kvp::gemm_resid_bf16(dqkv, wst, gres, true, gb, (float*)dx, M, h, np, st), "dX GEMM");
+             })))
+            return rc;
     }
     return ok();
 }

@@ -267,6 +267,48 @@ def test_workspace_and_call_checks():
     assert e.value.code == kb.KVP_E_CAPACITY
 
 
+def test_training_entry_points_host_checks():
+    # bf16 model with one consumer; no device memory is touched by these checks.
+    m = kb.Model(2, 256, 2, 1, 128, kb.KVP_DTYPE_BF16, [0, 0], max_batch=2, max_seq=200,
+                 kv_capacity=256)
+    n1 = m.kvp_train_saved_size(2, 200)
+    # Per layer: Q, O, X [400][256] bf16 and the log-sum-exp [2][2][256] fp32.
+    assert n1 == 2 * (3 * 400 * 256 * 2 + 2 * 2 * 256 * 4)
+    assert m.kvp_workspace_size(kb.KVP_PHASE_BACKWARD, 2, 200) > 0
+    with pytest.raises(kb.KvpError) as e:
+        m.kvp_train_saved_size(3, 200)
+    assert e.value.code == kb.KVP_E_CAPACITY
+    with pytest.raises(kb.KvpError) as e:      # a consumer has no dW_K, dW_V
+        m.kvp_set_layer_grads(1, 16, 32, 48, 64)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    with pytest.raises(kb.KvpError):           # a producer needs them
+        m.kvp_set_layer_grads(0, 16, 0, 0, 64)
+    with pytest.raises(kb.KvpError) as e:      # gradient buffers never set
+        m.kvp_backward(16, 32, 48, 2, 200, 64, n1, 80, 1 << 40)
+    assert e.value.code == kb.KVP_E_STATE
+    m.kvp_set_layer_grads(0, 16, 32, 48, 64)
+    m.kvp_set_layer_grads(1, 16, 0, 0, 64)
+    with pytest.raises(kb.KvpError) as e:      # dx aliases dy
+        m.kvp_backward(16, 32, 32, 2, 200, 64, n1, 80, 1 << 40)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    with pytest.raises(kb.KvpError) as e:      # short saved buffer
+        m.kvp_backward(16, 32, 48, 2, 200, 64, n1 - 1, 80, 1 << 40)
+    assert e.value.code == kb.KVP_E_WORKSPACE
+    with pytest.raises(kb.KvpError) as e:      # short workspace
+        m.kvp_backward(16, 32, 48, 2, 200, 64, n1, 80, 16)
+    assert e.value.code == kb.KVP_E_WORKSPACE
+    m.close()
+    # fp32 models have no training path.
+    f = kb.Model(1, 64, 1, 1, 64, kb.KVP_DTYPE_FP32, [0], max_batch=1, max_seq=8, kv_capacity=8)
+    with pytest.raises(kb.KvpError) as e:
+        f.kvp_train_saved_size(1, 8)
+    assert e.value.code == kb.KVP_E_SHAPE
+    with pytest.raises(kb.KvpError) as e:
+        f.kvp_workspace_size(kb.KVP_PHASE_BACKWARD, 1, 8)
+    assert e.value.code == kb.KVP_E_SHAPE
+    f.close()
+
+
 def test_calibration_entry_points_reject_bad_arguments():
     """include/kvp_calib.h: argument checks happen on the host, before any launch."""
     L = kb.lib()
