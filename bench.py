@@ -12,6 +12,8 @@ A step is one pass of the whole path over one batch of synthetic input:
 * decode: one new token per sequence through the 32-layer d_model 4096 GQA
   stack (batch 64, 32768-token caches, odd layers share) in tokens/s and
   algorithmic HBM GB/s.
+* train: forward with saved activations plus the backward of the same 8-layer
+  stage (dX and every weight gradient), in TFLOP/s of 3x the forward's FLOPs.
 The JSON line also carries the roofline of the dominant kernel (timed with HIP
 events on its own stream) against the datasheet peak and against the peak this
 device measurably delivers (a bf16 matrix-core loop and a streaming read, run
@@ -58,6 +60,24 @@ def prefill_flops(w: ki.Workload, B: int, S: int, tau=None):
         out["flash_attn"] += 4 * B * w.a * w.d_h * pairs
         out["oproj_gemm"] += 2 * M * nq * w.h
     return out
+
+
+def backward_flops(w: ki.Workload, B: int, S: int, tau=None):
+    """Per-kind FLOPs of one stack backward.  Algorithmic: the projection gradients (dO, dW_O,
+    dW_QKV, dX: twice the forward projections) and the four attention products (dV, dP, dQ, dK:
+    twice the forward attention).  Executed by the attention kernels, over the causal pairs:
+    the dK/dV kernel recomputes S and runs dP, dV, dK (4 products), the dQ kernel recomputes S
+    and dP and runs dQ (3)."""
+    tau = w.tau if tau is None else tau
+    M = B * S
+    nq, nkv = w.a * w.d_h, w.g * w.d_h
+    unit = 2 * B * w.a * w.d_h * (S * (S + 1) // 2)     # one causal [S x S x d] product, all heads
+    gemm = 0
+    for l in range(w.L):
+        npj = nq + (2 * nkv if tau[l] == l else 0)
+        gemm += 2 * M * w.h * nq * 2 + 2 * M * w.h * npj * 2
+    return {"bwd_gemm": gemm, "bwd_attn_algorithmic": 4 * unit * w.L,
+            "bwd_attn_kv_executed": 4 * unit * w.L, "bwd_attn_q_executed": 3 * unit * w.L}
 
 
 def decode_bytes(w: ki.Workload, lens, tau=None):
@@ -167,6 +187,86 @@ def bench_prefill(w: ki.Workload, steps: int, warmup: int, tau=None):
     del st, x, y, ws
     torch.cuda.empty_cache()
     return ms, prof, ok
+
+
+def bench_train(w: ki.Workload, steps: int, warmup: int):
+    """One training step of the stack: kvp_train_forward (the prefill kernels, keeping Q, O, the
+    layer inputs and the log-sum-exp) then kvp_backward (dX and every weight gradient, fp32)."""
+    import torch
+    from kvp_inputs import device as kd
+    from paper_2608_15943_amd import binding as kb
+    B, S = w.batch, w.seq
+    st = Stack(w, B, S, w.kv_capacity)
+    m = st.model
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device="cuda")
+    kd.fill_prefill_x(w, x.data_ptr(), B, S)
+    y = torch.empty_like(x)
+    dy = torch.empty((B, S, w.h), dtype=torch.float32, device="cuda")
+    kd.fill_prefill_dy(w, dy.data_ptr(), B, S)
+    dx = torch.empty_like(dy)
+    grads = []
+    for l in range(w.L):
+        prod = w.tau[l] == l
+        g = {"q": torch.empty((w.a * w.d_h, w.h), device="cuda"),
+             "o": torch.empty((w.h, w.a * w.d_h), device="cuda")}
+        if prod:
+            g["k"] = torch.empty((w.g * w.d_h, w.h), device="cuda")
+            g["v"] = torch.empty((w.g * w.d_h, w.h), device="cuda")
+        m.kvp_set_layer_grads(l, g["q"].data_ptr(), g["k"].data_ptr() if prod else 0,
+                              g["v"].data_ptr() if prod else 0, g["o"].data_ptr())
+        grads.append(g)
+    nf = m.kvp_workspace_size(kb.KVP_PHASE_PREFILL, B, S)
+    nb = m.kvp_workspace_size(kb.KVP_PHASE_BACKWARD, B, S)
+    ns = m.kvp_train_saved_size(B, S)
+    ws = torch.empty(max(nf, nb), dtype=torch.uint8, device="cuda")
+    saved = torch.empty(ns, dtype=torch.uint8, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    log(f"[bench] train {w.name}: saved {ns / 2**30:.2f} GiB, backward workspace {nb / 2**30:.2f} GiB")
+
+    def run():
+        m.kvp_train_forward(x.data_ptr(), y.data_ptr(), B, S, saved.data_ptr(), ns, ws.data_ptr(), nf,
+                            stream)
+        m.kvp_backward(x.data_ptr(), dy.data_ptr(), dx.data_ptr(), B, S, saved.data_ptr(), ns,
+                       ws.data_ptr(), nb, stream)
+
+    ms, prof = time_steps(run, m, steps, warmup)
+    ok = bool(torch.isfinite(dx).all().item()) and all(
+        bool(torch.isfinite(t).all().item()) for g in grads for t in g.values())
+    del st, x, y, dy, dx, grads, ws, saved
+    torch.cuda.empty_cache()
+    return ms, prof, ok
+
+
+def train_entry(w: ki.Workload, steps: int, warmup: int):
+    ms, prof, ok = bench_train(w, steps, warmup)
+    ff = prefill_flops(w, w.batch, w.seq)
+    bf = backward_flops(w, w.batch, w.seq)
+    fwd_flops = sum(ff.values())
+    algo = fwd_flops + bf["bwd_gemm"] + bf["bwd_attn_algorithmic"]     # = 3 x forward
+    kern = {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof.items()}
+    tot = {k: t / steps for k, (n, t) in prof.items()}                # ms per step per kind
+    bwd_ms = sum(v for k, v in tot.items() if k.startswith("bwd_"))
+    rates = {
+        "bwd_attn_kv": round(bf["bwd_attn_kv_executed"] / (tot["bwd_attn_kv"] * 1e-3) / 1e12, 1),
+        "bwd_attn_q": round(bf["bwd_attn_q_executed"] / (tot["bwd_attn_q"] * 1e-3) / 1e12, 1),
+        "bwd_attn_algorithmic": round(bf["bwd_attn_algorithmic"] /
+                                      ((tot["bwd_attn_kv"] + tot["bwd_attn_q"]) * 1e-3) / 1e12, 1),
+        "bwd_gemm": round(bf["bwd_gemm"] / (tot["bwd_gemm"] * 1e-3) / 1e12, 1),
+    }
+    out = {"workload": w.name, "ms_per_step": round(ms, 4),
+           "tflops": round(algo / (ms * 1e-3) / 1e12, 2),
+           "flops_per_step": algo, "forward_flops": fwd_flops,
+           "backward_ms_per_step_kernels": round(bwd_ms, 4),
+           "backward_tflops_kernels": round((bf["bwd_gemm"] + bf["bwd_attn_algorithmic"]) /
+                                            (bwd_ms * 1e-3) / 1e12, 1),
+           "per_kernel_tflops": rates, "per_kernel_roofline": kernel_fracs(rates),
+           "finite": ok, "kernels": kern,
+           "note": "step = kvp_train_forward + kvp_backward; TFLOP/s counts 3x the forward's "
+                   "algorithmic FLOPs; attention kernels' figures count the products they execute "
+                   "(S and dP recomputed), bwd_attn_algorithmic counts dV, dP, dQ, dK once"}
+    log(f"[bench] train {ms:.3f} ms/step, {out['tflops']} TFLOP/s; backward kernels {bwd_ms:.3f} ms, "
+        f"rates {rates}")
+    return out
 
 
 def bench_decode(w: ki.Workload, steps: int, warmup: int, alias_of=None):
@@ -393,7 +493,9 @@ def main():
                     help="skip the 70B-shaped prefill and the ragged 128K decode lines")
     ap.add_argument("--no-calib", action="store_true",
                     help="skip the achievable-peak calibration (no frac_achievable figures)")
-    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib"],
+    ap.add_argument("--no-train", action="store_true", help="skip the training-step line")
+    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib",
+                                       "train"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
@@ -425,6 +527,8 @@ def main():
             out = decode_entry(ki.decode_32k(), steps_d, warm_d)
         elif args.only == "decode_128k":
             out = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
+        elif args.only == "train":
+            out = train_entry(ki.stage_share_prefill(), steps_d, warm_d)
         else:
             w = ki.stage_share_prefill()
             ms, prof, finite = bench_prefill(w, args.steps, args.warmup)
@@ -476,6 +580,9 @@ def main():
 
     if not args.no_extra:
         result["prefill_70b_stage"] = bench_70b(args.steps, args.warmup)
+
+    if not args.no_train:
+        result["train"] = train_entry(w, max(3, args.steps // 2), max(1, args.warmup // 2))
 
     if not args.no_decode:
         steps_d, warm_d = max(3, args.steps // 2), max(1, args.warmup // 2)

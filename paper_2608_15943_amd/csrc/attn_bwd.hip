@@ -13,7 +13,7 @@
 //   attn_bwd_prep    D, and the transposed copies dO^T, Q^T, O^T the products over
 //                    the query axis need (each [a*128][B*Sp], Sp = S rounded up to 64,
 //                    zero past S).
-//   flash_bwd_kv     one workgroup per (sequence, KV head, 128 keys); loops over the r
+//   flash_bwd_kv     one workgroup per (sequence, KV head, 256 keys); loops over the r
 //                    query heads of the group and the query blocks at or after its
 //                    keys; dK, dV accumulate in registers.
 //   flash_bwd_q      one workgroup per (sequence, head, 256 queries); loops over the
@@ -187,16 +187,17 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const uint16_t* __re
 }
 
 // ---------------------------------------------------------------------------
-// dK, dV.  Workgroup = 4 waves = 128 keys of one (sequence, KV head); wave w owns keys
+// dK, dV.  Workgroup = 8 waves = 256 keys of one (sequence, KV head); wave w owns keys
 // 32 w .. 32 w + 31 (one accumulator column each for dK and dV per lane: 4 blocks of
-// 32 dims).  Per step: one block of 64 queries of one of the r heads, staged in LDS as
-// Q, dO ([64][128], 256-byte rows, chunk c at c ^ (row & 15)) and Q^T, dO^T ([128][64],
-// 128-byte rows, chunk c at c ^ ((row >> 1) & 7)), plus the 64 log-sum-exp and D values;
-// double buffered (2 x 64.5 KB).
-//   S  [64 q x 32 k] = Q K^T     (A = Q rows, permuted; B = K, registers)
-//   dP [64 q x 32 k] = dO V^T    (A = dO rows, same order; B = V, registers)
-//   dV [32 k x 128]  += P^T dO   (A = P from the S registers; B = dO^T from LDS)
-//   dK [32 k x 128]  += dS^T Q   (A = dS; B = Q^T)
+// 32 dims); two waves per SIMD.  The keys' V rows stay in LDS for the whole kernel
+// ([256][128], 64 KB); K is held in registers.  Per step: one block of 32 queries of one
+// of the r heads, staged in LDS as Q, dO ([32][128], 256-byte rows, chunk c at
+// c ^ (row & 15)) and Q^T, dO^T ([128][32], 64-byte rows, chunk c at c ^ ((row >> 2) & 3)),
+// plus the 32 log-sum-exp and D values; double buffered (2 x 32.25 KB).
+//   S  [32 q x 32 k] = Q K^T     (A = Q rows, permuted; B = K, registers)
+//   dP [32 q x 32 k] = dO V^T    (A = dO rows, same order; B = V rows, LDS)
+//   dV [32 k x 128]  += P^T dO   (A = P from the S registers; B = dO^T, LDS)
+//   dK [32 k x 128]  += dS^T Q   (A = dS; B = Q^T, LDS)
 // ---------------------------------------------------------------------------
 struct KvArgs {
     const uint16_t* q;      // [B*S][a*128] post-RoPE Q of the layer
@@ -206,7 +207,7 @@ struct KvArgs {
     const float* lse;       // [B][a][Sp], log2 domain
     const float* dsum;      // [B][a][Sp]
     const uint16_t* kc;     // producer K slot [Bmax][g][cap][128]
-    const uint16_t* vc;     // producer V slot [Bmax][g][128][cap]
+    const uint16_t* vr;     // producer V rows [B*g][Sp][128], zero past S
     const float2* rope;     // [S][64]
     const float* acc_in_k;  // [B][g][S][128] or null
     const float* acc_in_v;
@@ -219,14 +220,15 @@ struct KvArgs {
     float scale_log2, scale;
 };
 
-constexpr int KV_BQ = 64, KV_NT = 256;
+constexpr int KV_BQ = 32, KV_BK = 256, KV_NT = 512;
 
-__global__ __launch_bounds__(KV_NT, 1) void flash_bwd_kv_kernel(KvArgs A) {
+__global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
+    __shared__ u32x4 lvk[KV_BK * 16];          // V rows of the workgroup's keys
     __shared__ u32x4 lq[2][KV_BQ * 16];
     __shared__ u32x4 ldo_[2][KV_BQ * 16];
-    __shared__ u32x4 lqt[2][D * 8];
-    __shared__ u32x4 ldot[2][D * 8];
-    __shared__ float lstat[2][2][KV_BQ];   // [stage][lse, D][query]
+    __shared__ u32x4 lqt[2][D * 4];
+    __shared__ u32x4 ldot[2][D * 4];
+    __shared__ float lstat[2][2 * KV_BQ];      // [stage][lse 0..31, D 0..31]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, hi = lane >> 5;
@@ -234,32 +236,33 @@ __global__ __launch_bounds__(KV_NT, 1) void flash_bwd_kv_kernel(KvArgs A) {
     const int kb = blockIdx.x / G, grp = blockIdx.x - kb * G;   // heaviest key blocks first
     const int b = grp / A.g, kvh = grp - b * A.g;
     const int r = A.a / A.g;
-    const int k0w = kb * 128 + 32 * wave;
+    const int k0w = kb * KV_BK + 32 * wave;
     const int key = k0w + l32;                 // the key whose column this lane holds
     const bool kvalid = key < A.S;
+    const size_t plane = (size_t)b * A.g + kvh;
 
-    // K and V of the lane's key, as B operands (8 dims per 16-wide step); zero past S.
-    bf16x8 kf[8], vf[8];
+    // V rows of the 256 keys into LDS (rows past Sp clamped: their keys are masked).
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int row = 32 * wave + 4 * j + (lane >> 4);
+        const int c = (lane & 15) ^ (row & 15);
+        const int pos = min(kb * KV_BK + row, A.Sp - 1);
+        load_lds16(A.vr + (plane * A.Sp + pos) * D + 8 * c, &lvk[(32 * wave + 4 * j) * 16]);
+    }
+    // K of the lane's key as the B operand of S (8 dims per 16-wide step); zero past S.
+    bf16x8 kf[8];
     {
-        const uint16_t* krow = A.kc + (((size_t)b * A.g + kvh) * A.cap + (kvalid ? key : 0)) * D + 8 * hi;
-        const uint16_t* vcol = A.vc + ((size_t)b * A.g + kvh) * D * A.cap + (kvalid ? key : 0);
+        const uint16_t* krow = A.kc + (plane * A.cap + (kvalid ? key : 0)) * D + 8 * hi;
 #pragma unroll
         for (int ks = 0; ks < 8; ++ks) {
             u32x4 kw = *(const u32x4*)(krow + 16 * ks);
-            uint32_t vw[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                const int d = 16 * ks + 8 * hi + 2 * e;
-                vw[e] = (uint32_t)vcol[(size_t)d * A.cap] | ((uint32_t)vcol[(size_t)(d + 1) * A.cap] << 16);
-            }
             if (!kvalid) kw = u32x4{0, 0, 0, 0};
             kf[ks] = as_bf16x8(kw);
-            vf[ks] = as_bf16x8(kvalid ? u32x4{vw[0], vw[1], vw[2], vw[3]} : u32x4{0, 0, 0, 0});
         }
     }
 
     const int nqb = A.Sp / KV_BQ;
-    const int qb_lo = min(2 * kb, nqb);
+    const int qb_lo = min(kb * (KV_BK / KV_BQ), nqb);
     const int nq_h = nqb - qb_lo;               // query blocks per head
     const int n_it = r * nq_h;
     const size_t ld = (size_t)A.a * D, ldt = (size_t)A.B * A.Sp;
@@ -267,25 +270,23 @@ __global__ __launch_bounds__(KV_NT, 1) void flash_bwd_kv_kernel(KvArgs A) {
     auto issue = [&](int it, int stg) {
         const int head = kvh * r + it / nq_h;
         const int qb0 = (qb_lo + it % nq_h) * KV_BQ;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int row = 16 * wave + 4 * j + (lane >> 4);
+        {
+            const int row = 4 * wave + (lane >> 4);
             const int c = (lane & 15) ^ (row & 15);
             const size_t src = ((size_t)b * A.S + min(qb0 + row, A.S - 1)) * ld + head * D + 8 * c;
-            load_lds16(A.q + src, &lq[stg][(16 * wave + 4 * j) * 16]);
-            load_lds16(A.dO + src, &ldo_[stg][(16 * wave + 4 * j) * 16]);
+            load_lds16(A.q + src, &lq[stg][(4 * wave) * 16]);
+            load_lds16(A.dO + src, &ldo_[stg][(4 * wave) * 16]);
         }
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int d = 32 * wave + 8 * j + (lane >> 3);
-            const int c = (lane & 7) ^ ((d >> 1) & 7);
+        {
+            const int d = 16 * wave + (lane >> 2);
+            const int c = (lane & 3) ^ ((d >> 2) & 3);
             const size_t src = (size_t)(head * D + d) * ldt + (size_t)b * A.Sp + qb0 + 8 * c;
-            load_lds16(A.qt + src, &lqt[stg][(32 * wave + 8 * j) * 8]);
-            load_lds16(A.dOt + src, &ldot[stg][(32 * wave + 8 * j) * 8]);
+            load_lds16(A.qt + src, &lqt[stg][(16 * wave) * 4]);
+            load_lds16(A.dOt + src, &ldot[stg][(16 * wave) * 4]);
         }
-        if (wave < 2) {
-            const float* src = (wave == 0 ? A.lse : A.dsum) + ((size_t)b * A.a + head) * A.Sp + qb0 + lane;
-            load_lds4(src, &lstat[stg][wave][0]);
+        if (wave == 0) {
+            const float* src = (hi == 0 ? A.lse : A.dsum) + ((size_t)b * A.a + head) * A.Sp + qb0 + l32;
+            load_lds4(src, &lstat[stg][0]);
         }
     };
 
@@ -305,47 +306,45 @@ __global__ __launch_bounds__(KV_NT, 1) void flash_bwd_kv_kernel(KvArgs A) {
         if (it + 1 < n_it) issue(it + 1, stg ^ 1);
         const int qb0 = (qb_lo + it % nq_h) * KV_BQ;
         if (qb0 + KV_BQ - 1 < k0w) continue;      // every query of the block precedes the wave's keys
-        f32x16 s[2], dp[2];
+        f32x16 s = f32x16{}, dp = f32x16{};
+        const int vr_ = 32 * wave + l32;          // this lane's key row in the V tile
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            s[rb] = f32x16{};
-            dp[rb] = f32x16{};
-            const int row = 32 * rb + rsw;
-#pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
-                const int c = (2 * ks + hi) ^ (row & 15);
-                s[rb] = mfma32x32x16(as_bf16x8(lq[stg][row * 16 + c]), kf[ks], s[rb]);
-                dp[rb] = mfma32x32x16(as_bf16x8(ldo_[stg][row * 16 + c]), vf[ks], dp[rb]);
-            }
+        for (int ks = 0; ks < 8; ++ks) {
+            const int c = (2 * ks + hi) ^ (rsw & 15);
+            s = mfma32x32x16(as_bf16x8(lq[stg][rsw * 16 + c]), kf[ks], s);
+            const bf16x8 vf = as_bf16x8(lvk[vr_ * 16 + ((2 * ks + hi) ^ (vr_ & 15))]);
+            dp = mfma32x32x16(as_bf16x8(ldo_[stg][rsw * 16 + c]), vf, dp);
         }
-        // Register i of block rb holds query qb0 + 32 rb + 16 (i / 8) + 8 hi + i % 8.
-        bf16x8 pa[4], da[4];
+        // Register i holds query qb0 + 16 (i / 8) + 8 hi + i % 8.
+        bf16x8 pa[2], da[2];
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int h = 0; h < 2; ++h) {
+            const int qo = 16 * h + 8 * hi;
+            // Branch-free: the exponent is computed for every entry (masked ones may be
+            // garbage) and the mask selects 0; the 8 statistics are two 16-byte reads each.
+            const f32x4 l0 = *(const f32x4*)&lstat[stg][qo], l1 = *(const f32x4*)&lstat[stg][qo + 4];
+            const f32x4 d0 = *(const f32x4*)&lstat[stg][KV_BQ + qo], d1 = *(const f32x4*)&lstat[stg][KV_BQ + qo + 4];
+            float pe[8], de[8];
 #pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int qo = 32 * rb + 16 * h + 8 * hi;
-                float pe[8], de[8];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const int qi = qb0 + qo + k;
-                    const float lse = lstat[stg][0][qo + k], dd = lstat[stg][1][qo + k];
-                    const bool vis = key <= qi && qi < A.S;
-                    const float p = vis ? __builtin_amdgcn_exp2f(fmaf(s[rb][8 * h + k], A.scale_log2, -lse)) : 0.f;
-                    pe[k] = p;
-                    de[k] = vis ? p * (dp[rb][8 * h + k] - dd) : 0.f;
-                }
-                pa[2 * rb + h] = pack8(pe);
-                da[2 * rb + h] = pack8(de);
+            for (int k = 0; k < 8; ++k) {
+                const int qi = qb0 + qo + k;
+                const float lse = k < 4 ? l0[k] : l1[k - 4], dd = k < 4 ? d0[k] : d1[k - 4];
+                const bool vis = key <= qi && qi < A.S;
+                const float e = __builtin_amdgcn_exp2f(fmaf(s[8 * h + k], A.scale_log2, -lse));
+                pe[k] = vis ? e : 0.f;
+                de[k] = vis ? e * (dp[8 * h + k] - dd) : 0.f;
             }
+            pa[h] = pack8(pe);
+            da[h] = pack8(de);
+        }
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+        for (int h = 0; h < 2; ++h)
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
                 const int d = 32 * nb + l32;
-                const int ch = (2 * c + hi) ^ ((d >> 1) & 7);
-                dv[nb] = mfma32x32x16(pa[c], as_bf16x8(ldot[stg][d * 8 + ch]), dv[nb]);
-                dk[nb] = mfma32x32x16(da[c], as_bf16x8(lqt[stg][d * 8 + ch]), dk[nb]);
+                const int ch = (2 * h + hi) ^ ((d >> 2) & 3);
+                dv[nb] = mfma32x32x16(pa[h], as_bf16x8(ldot[stg][d * 4 + ch]), dv[nb]);
+                dk[nb] = mfma32x32x16(da[h], as_bf16x8(lqt[stg][d * 4 + ch]), dk[nb]);
             }
     }
 
@@ -522,8 +521,8 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
                 for (int k = 0; k < 8; ++k) {
                     const int kk = t0 + 32 * mb + 16 * h + 8 * hi + k;
                     const bool vis = kk <= ql && ql < A.S;
-                    const float p = vis ? __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + k], A.scale_log2, -lse)) : 0.f;
-                    de[k] = vis ? p * (dp[mb][8 * h + k] - dd) : 0.f;
+                    const float e = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + k], A.scale_log2, -lse));
+                    de[k] = vis ? e * (dp[mb][8 * h + k] - dd) : 0.f;
                 }
                 db_[2 * mb + h] = pack8(de);
             }
@@ -615,13 +614,13 @@ hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, const uint1
 hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
     KvArgs A;
     A.q = p.q; A.qt = p.qt; A.dO = p.dO; A.dOt = p.dOt; A.lse = p.lse; A.dsum = p.dsum;
-    A.kc = p.kc; A.vc = p.vc; A.rope = p.rope;
+    A.kc = p.kc; A.vr = p.vr; A.rope = p.rope;
     A.acc_in_k = p.acc_in_k; A.acc_in_v = p.acc_in_v; A.acc_out_k = p.acc_out_k; A.acc_out_v = p.acc_out_v;
     A.out = p.out; A.outT = p.outT; A.ldo = p.ldo; A.col_k = p.col_k; A.col_v = p.col_v;
     A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-    const int nkb = (p.S + 127) / 128;
+    const int nkb = (p.S + KV_BK - 1) / KV_BK;
     hipLaunchKernelGGL(flash_bwd_kv_kernel, dim3(nkb * p.B * p.g), dim3(KV_NT), 0, st, A);
     return hipGetLastError();
 }

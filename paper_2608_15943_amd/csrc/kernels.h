@@ -70,8 +70,8 @@ struct AttnBwdKv {
     const uint16_t* dOt;
     const float* lse;
     const float* dsum;
-    const uint16_t* kc;
-    const uint16_t* vc;
+    const uint16_t* kc;     // producer K slot
+    const uint16_t* vr;     // producer V rows [B*g][Sp][128], zero past S
     const float2* rope;
     const float* acc_in_k;
     const float* acc_in_v;

@@ -891,7 +891,7 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         {
             kvp::AttnBwdKv a{};
             a.q = Ql; a.qt = qt; a.dO = dO; a.dOt = dOt; a.lse = lse; a.dsum = dsum;
-            a.kc = (const uint16_t*)Pl.kc; a.vc = (const uint16_t*)Pl.vc; a.rope = rope;
+            a.kc = (const uint16_t*)Pl.kc; a.vr = vr; a.rope = rope;
             const int slot = w.acc_slot[p];
             float* ak = slot >= 0 ? acc + (size_t)slot * 2 * w.acc_plane : nullptr;
             float* av = slot >= 0 ? ak + w.acc_plane : nullptr;
