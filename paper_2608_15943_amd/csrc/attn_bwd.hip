@@ -10,9 +10,8 @@
 // -pos * theta) is applied to dQ and dK in the epilogues, before any accumulation.
 //
 // Kernels:
-//   attn_bwd_prep    D, and the transposed copies dO^T, Q^T, O^T the products over
-//                    the query axis need (each [a*128][B*Sp], Sp = S rounded up to 64,
-//                    zero past S).
+//   attn_bwd_prep    D, and O^T for the dW_O product ([a*128][Mp], column = token,
+//                    Mp = B*S rounded up to 64, zero tail).
 //   flash_bwd_kv     one workgroup per (sequence, KV head, 256 keys); loops over the r
 //                    query heads of the group and the query blocks at or after its
 //                    keys; dK, dV accumulate in registers.
@@ -25,7 +24,9 @@
 // column.  The first product of each kernel reads its A rows in a permuted order (bits 2
 // and 3 of the row swapped), so that the 8 values a lane holds for each 16-wide step of
 // the second product are 8 consecutive positions: P and dS feed the next products
-// straight from registers, and the other operand is one 16-byte LDS read.
+// straight from registers.  Operands that run along a staged tile's rows (dO, Q and V^T
+// for dV, dK and dP; K and V^T in the dQ kernel) are read with the LDS transpose read of
+// gfx950, so every tile is staged once, in the layout it has in memory.
 #include <math.h>
 
 #include <algorithm>
@@ -60,6 +61,50 @@ __device__ __forceinline__ bf16x8 pack8(const float* e) {
     w[2] = pack2bf(e[4], e[5]);
     w[3] = pack2bf(e[6], e[7]);
     return as_bf16x8(w);
+}
+
+typedef short v4i16 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
+
+// Staged tiles use a sub-tiled LDS layout: an NR x NC bf16 tile is stored as NC / 32 blocks
+// of 32 columns, each NR rows of 64 bytes; 16-byte chunk k (0..3) of row r of a block sits
+// at position k ^ ((r >> 2) & 3).  A column-block or 16-row offset is then a constant byte
+// offset (so every read below is one lane register plus an immediate), and 16 consecutive
+// rows of one chunk column cover all 64 banks.
+template <int NR>
+__device__ __forceinline__ int sub_off(int r, int c) {
+    return (c >> 5) * (NR * 64) + r * 64 + ((((c >> 3) & 3) ^ ((r >> 2) & 3)) << 4) + ((c & 7) << 1);
+}
+
+// One 1 KB direct load (16 bytes per lane) of rows 16 q .. 16 q + 15 of column block sb:
+// lane i fetches the global chunk that belongs at position i % 4 of row 16 q + i / 4.
+// Returns the chunk index (0..3) within the block; the caller supplies the global row.
+__device__ __forceinline__ int sub_chunk(int lane) { return (lane & 3) ^ ((lane >> 4) & 3); }
+
+// 8 consecutive columns c .. c + 7 (c % 8 == 0) of row r: one 16-byte read.
+template <int NR>
+__device__ __forceinline__ bf16x8 row8(const u32x4* tile, int r, int c) {
+    return *(const bf16x8*)((const char*)tile + sub_off<NR>(r, c));
+}
+
+// Operand fragment taken along a tile's rows: lane (n = lane % 32, hi = lane / 32) receives
+// tile[r0 + 8 hi + j][c0 + n], j = 0..7 (with PERM, column c0 + swap_b23(n)); r0 % 16 == 0
+// and c0 % 32 == 0.  Two ds_read_b64_tr_b16: in each group of 16 lanes, lane 4 a + e
+// receives element e of the 8 bytes addressed by lanes a, a + 4, a + 8, a + 12 of the group,
+// so lane i of a group addresses row r0 + 8 hi + i / 4 (+ 4 for the second read) at the
+// 4-column block that the result lanes with a = i % 4 need.
+template <int NR, bool PERM>
+__device__ __forceinline__ bf16x8 tr_frag(const u32x4* tile, int r0, int c0, int lane) {
+    const int G = lane >> 4, src = lane & 15, a = src & 3;
+    const int ap = PERM ? (((a & 1) << 1) | (a >> 1)) : a;
+    const int col = 16 * (G & 1) + 4 * ap;            // < 32
+    const int row = 8 * (G >> 1) + (src >> 2);         // < 16
+    const char* base = (const char*)tile + (c0 >> 5) * (NR * 64) + r0 * 64;
+    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + sub_off<NR>(row, col)));
+    const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + sub_off<NR>(row + 4, col)));
+    typedef short v8i16 __attribute__((ext_vector_type(8)));
+    const v8i16 v = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
+    return __builtin_bit_cast(bf16x8, v);
 }
 
 // ---------------------------------------------------------------------------
@@ -118,38 +163,32 @@ __global__ __launch_bounds__(256) void reduce_planes_kernel(const float* __restr
 }
 
 // ---------------------------------------------------------------------------
-// D = rowsum(dO * O) and the transposed copies.  One workgroup per (sequence, head,
-// 64 positions); the three [64][128] tiles pass through LDS.
+// D = rowsum(dO * O) and O^T.  One workgroup per (64 tokens of the flattened B*S axis,
+// head); the O tile passes through LDS.  O^T is [a*128][Mp] with column = token, zero
+// for the tail [M, Mp).
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const uint16_t* __restrict__ dO,
                                                             const uint16_t* __restrict__ O,
-                                                            const uint16_t* __restrict__ Q,
                                                             float* __restrict__ dsum,
-                                                            uint16_t* __restrict__ dOt,
-                                                            uint16_t* __restrict__ Qt,
                                                             uint16_t* __restrict__ Ot, int B, int S,
-                                                            int Sp, int a) {
-    __shared__ uint16_t tile[3][64][136];   // rows of 128 values + 8 of padding
-    const int nst = Sp / 64;
-    const int st = blockIdx.x % nst, bh = blockIdx.x / nst;
-    const int b = bh / a, head = bh - b * a;
-    const int s0 = st * 64;
+                                                            int Sp, int Mp, int a) {
+    __shared__ uint16_t tile[64][136];   // rows of 128 values + 8 of padding
+    const int nmt = Mp / 64;
+    const int mt = blockIdx.x % nmt, head = blockIdx.x / nmt;
+    const int m0 = mt * 64, M = B * S;
     const int tid = threadIdx.x;
     const size_t ld = (size_t)a * D;
-    // Loads: thread t reads 4 x 16 bytes of row t / 4 (dims 32 (t % 4) .. + 31) of each tile.
+    // Loads: thread t reads 4 x 16 bytes of row t / 4 (dims 32 (t % 4) .. + 31).
     const int r = tid >> 2, q4 = tid & 3;
-    const int s = s0 + r;
+    const int m = m0 + r;
     float acc = 0.f;
-    if (s < S) {
-        const size_t off = ((size_t)b * S + s) * ld + head * D + 32 * q4;
+    if (m < M) {
+        const size_t off = (size_t)m * ld + head * D + 32 * q4;
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
             const u32x4 vd = *(const u32x4*)(dO + off + 8 * k);
             const u32x4 vo = *(const u32x4*)(O + off + 8 * k);
-            const u32x4 vq = *(const u32x4*)(Q + off + 8 * k);
-            *(u32x4*)&tile[0][r][32 * q4 + 8 * k] = vd;
-            *(u32x4*)&tile[1][r][32 * q4 + 8 * k] = vq;
-            *(u32x4*)&tile[2][r][32 * q4 + 8 * k] = vo;
+            *(u32x4*)&tile[r][32 * q4 + 8 * k] = vo;
 #pragma unroll
             for (int e = 0; e < 4; ++e) {
                 acc += __uint_as_float(vd[e] << 16) * __uint_as_float(vo[e] << 16);
@@ -158,77 +197,70 @@ __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const uint16_t* __re
         }
     } else {
 #pragma unroll
-        for (int k = 0; k < 4; ++k)
-#pragma unroll
-            for (int m = 0; m < 3; ++m) *(u32x4*)&tile[m][r][32 * q4 + 8 * k] = u32x4{0, 0, 0, 0};
+        for (int k = 0; k < 4; ++k) *(u32x4*)&tile[r][32 * q4 + 8 * k] = u32x4{0, 0, 0, 0};
     }
     acc += __shfl_xor(acc, 1);
     acc += __shfl_xor(acc, 2);
-    if (q4 == 0) dsum[((size_t)b * a + head) * Sp + s] = acc;
+    if (q4 == 0 && m < M) {
+        const int b = m / S, s = m - b * S;
+        dsum[((size_t)b * a + head) * Sp + s] = acc;
+    }
     __syncthreads();
-    // Stores: output row d (of the head's 128), 8 positions per 16-byte store; thread t
-    // writes rows t / 8 + 32 k, positions 8 (t % 8) .. + 7.
-    const size_t ldt = (size_t)B * Sp;
+    // Stores: O^T row d of the head, 8 tokens per 16-byte store; thread t writes rows
+    // t / 8 + 32 k, tokens 8 (t % 8) .. + 7.
     const int c8 = tid & 7;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
         const int d = (tid >> 3) + 32 * k;
-        const size_t off = (size_t)(head * D + d) * ldt + (size_t)b * Sp + s0 + 8 * c8;
+        uint32_t w[4];
 #pragma unroll
-        for (int m = 0; m < 3; ++m) {
-            uint32_t w[4];
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-                w[e] = (uint32_t)tile[m][8 * c8 + 2 * e][d] | ((uint32_t)tile[m][8 * c8 + 2 * e + 1][d] << 16);
-            uint16_t* dst = m == 0 ? dOt : (m == 1 ? Qt : Ot);
-            *(u32x4*)(dst + off) = u32x4{w[0], w[1], w[2], w[3]};
-        }
+        for (int e = 0; e < 4; ++e)
+            w[e] = (uint32_t)tile[8 * c8 + 2 * e][d] | ((uint32_t)tile[8 * c8 + 2 * e + 1][d] << 16);
+        *(u32x4*)(Ot + (size_t)(head * D + d) * Mp + m0 + 8 * c8) = u32x4{w[0], w[1], w[2], w[3]};
     }
 }
 
 // ---------------------------------------------------------------------------
 // dK, dV.  Workgroup = 8 waves = 256 keys of one (sequence, KV head); wave w owns keys
 // 32 w .. 32 w + 31 (one accumulator column each for dK and dV per lane: 4 blocks of
-// 32 dims); two waves per SIMD.  The keys' V rows stay in LDS for the whole kernel
-// ([256][128], 64 KB); K is held in registers.  Per step: one block of 32 queries of one
-// of the r heads, staged in LDS as Q, dO ([32][128], 256-byte rows, chunk c at
-// c ^ (row & 15)) and Q^T, dO^T ([128][32], 64-byte rows, chunk c at c ^ ((row >> 2) & 3)),
-// plus the 32 log-sum-exp and D values; double buffered (2 x 32.25 KB).
+// 32 dims); two waves per SIMD.  K of the lane's key is held in registers, V^T of the 256
+// keys in LDS ([128][256], 64 KB) for the whole kernel.  Per step: one block of 64
+// queries of one of the r heads, staged in LDS as Q and dO rows ([64][128]) plus their 64
+// log-sum-exp and D values; double buffered (2 x 32.5 KB); tiles in the sub-tiled layout.
+// Each 32-query half:
 //   S  [32 q x 32 k] = Q K^T     (A = Q rows, permuted; B = K, registers)
-//   dP [32 q x 32 k] = dO V^T    (A = dO rows, same order; B = V rows, LDS)
-//   dV [32 k x 128]  += P^T dO   (A = P from the S registers; B = dO^T, LDS)
-//   dK [32 k x 128]  += dS^T Q   (A = dS; B = Q^T, LDS)
+//   dP [32 q x 32 k] = dO V^T    (A = dO rows, same order; B = V^T tile along its rows)
+//   dV [32 k x 128]  += P^T dO   (A = P from the S registers; B = dO tile along its rows)
+//   dK [32 k x 128]  += dS^T Q   (A = dS; B = Q tile along its rows)
+// The operands taken along a tile's rows are transposed reads (tr_frag), so no transposed
+// copy of Q, dO or V is made.
 // ---------------------------------------------------------------------------
 struct KvArgs {
     const uint16_t* q;      // [B*S][a*128] post-RoPE Q of the layer
-    const uint16_t* qt;     // [a*128][B*Sp]
     const uint16_t* dO;     // [B*S][a*128]
-    const uint16_t* dOt;    // [a*128][B*Sp]
     const float* lse;       // [B][a][Sp], log2 domain
     const float* dsum;      // [B][a][Sp]
     const uint16_t* kc;     // producer K slot [Bmax][g][cap][128]
-    const uint16_t* vr;     // producer V rows [B*g][Sp][128], zero past S
+    const uint16_t* vc;     // producer V slot [Bmax][g][128][cap]
     const float2* rope;     // [S][64]
     const float* acc_in_k;  // [B][g][S][128] or null
     const float* acc_in_v;
     float* acc_out_k;       // may alias acc_in_*
     float* acc_out_v;
     uint16_t* out;          // final rows [B*S][ldo] or null; dK at col_k + kvh*128, dV at col_v
-    uint16_t* outT;         // final transposed [*][B*Sp] or null, same columns as rows
+    uint16_t* outT;         // final transposed [*][Mp] (column = token) or null
     int ldo, col_k, col_v;
-    int B, S, Sp, a, g, cap;
+    int B, S, Sp, Mp, a, g, cap;
     float scale_log2, scale;
 };
 
-constexpr int KV_BQ = 32, KV_BK = 256, KV_NT = 512;
+constexpr int KV_BQ = 64, KV_BK = 256, KV_NT = 512;
 
 __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
-    __shared__ u32x4 lvk[KV_BK * 16];          // V rows of the workgroup's keys
+    __shared__ u32x4 lvt[D * 32];              // V^T of the workgroup's keys, 512-byte rows
     __shared__ u32x4 lq[2][KV_BQ * 16];
     __shared__ u32x4 ldo_[2][KV_BQ * 16];
-    __shared__ u32x4 lqt[2][D * 4];
-    __shared__ u32x4 ldot[2][D * 4];
-    __shared__ float lstat[2][2 * KV_BQ];      // [stage][lse 0..31, D 0..31]
+    __shared__ float lstat[2][2 * KV_BQ];      // [stage][lse 0..63, D 0..63]
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, hi = lane >> 5;
@@ -241,13 +273,14 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
     const bool kvalid = key < A.S;
     const size_t plane = (size_t)b * A.g + kvh;
 
-    // V rows of the 256 keys into LDS (rows past Sp clamped: their keys are masked).
+    // V^T of the 256 keys into LDS: wave w fills column block w (its own keys).  Chunks
+    // past the slot are clamped: their keys lie beyond S, so their dP columns are masked.
+    const int ch = sub_chunk(lane);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int row = 32 * wave + 4 * j + (lane >> 4);
-        const int c = (lane & 15) ^ (row & 15);
-        const int pos = min(kb * KV_BK + row, A.Sp - 1);
-        load_lds16(A.vr + (plane * A.Sp + pos) * D + 8 * c, &lvk[(32 * wave + 4 * j) * 16]);
+    for (int q = 0; q < 8; ++q) {
+        const int row = 16 * q + (lane >> 2);
+        const int k0 = min(kb * KV_BK + 32 * wave + 8 * ch, A.cap - 8);
+        load_lds16(A.vc + (plane * D + row) * A.cap + k0, (char*)lvt + wave * (D * 64) + q * 1024);
     }
     // K of the lane's key as the B operand of S (8 dims per 16-wide step); zero past S.
     bf16x8 kf[8];
@@ -265,28 +298,22 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
     const int qb_lo = min(kb * (KV_BK / KV_BQ), nqb);
     const int nq_h = nqb - qb_lo;               // query blocks per head
     const int n_it = r * nq_h;
-    const size_t ld = (size_t)A.a * D, ldt = (size_t)A.B * A.Sp;
+    const size_t ld = (size_t)A.a * D;
 
     auto issue = [&](int it, int stg) {
         const int head = kvh * r + it / nq_h;
         const int qb0 = (qb_lo + it % nq_h) * KV_BQ;
-        {
-            const int row = 4 * wave + (lane >> 4);
-            const int c = (lane & 15) ^ (row & 15);
-            const size_t src = ((size_t)b * A.S + min(qb0 + row, A.S - 1)) * ld + head * D + 8 * c;
-            load_lds16(A.q + src, &lq[stg][(4 * wave) * 16]);
-            load_lds16(A.dO + src, &ldo_[stg][(4 * wave) * 16]);
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+            const int t = 2 * wave + j, sb = t >> 2, q = t & 3;
+            const int row = 16 * q + (lane >> 2);
+            const size_t src = ((size_t)b * A.S + min(qb0 + row, A.S - 1)) * ld + head * D + 32 * sb + 8 * ch;
+            load_lds16(A.q + src, (char*)lq[stg] + sb * (KV_BQ * 64) + q * 1024);
+            load_lds16(A.dO + src, (char*)ldo_[stg] + sb * (KV_BQ * 64) + q * 1024);
         }
-        {
-            const int d = 16 * wave + (lane >> 2);
-            const int c = (lane & 3) ^ ((d >> 2) & 3);
-            const size_t src = (size_t)(head * D + d) * ldt + (size_t)b * A.Sp + qb0 + 8 * c;
-            load_lds16(A.qt + src, &lqt[stg][(16 * wave) * 4]);
-            load_lds16(A.dOt + src, &ldot[stg][(16 * wave) * 4]);
-        }
-        if (wave == 0) {
-            const float* src = (hi == 0 ? A.lse : A.dsum) + ((size_t)b * A.a + head) * A.Sp + qb0 + l32;
-            load_lds4(src, &lstat[stg][0]);
+        if (wave < 2) {
+            const float* src = (wave == 0 ? A.lse : A.dsum) + ((size_t)b * A.a + head) * A.Sp + qb0 + lane;
+            load_lds4(src, &lstat[stg][KV_BQ * wave]);
         }
     };
 
@@ -305,47 +332,48 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
         __syncthreads();                          // tile it landed; tile it - 1 fully read
         if (it + 1 < n_it) issue(it + 1, stg ^ 1);
         const int qb0 = (qb_lo + it % nq_h) * KV_BQ;
-        if (qb0 + KV_BQ - 1 < k0w) continue;      // every query of the block precedes the wave's keys
-        f32x16 s = f32x16{}, dp = f32x16{};
-        const int vr_ = 32 * wave + l32;          // this lane's key row in the V tile
 #pragma unroll
-        for (int ks = 0; ks < 8; ++ks) {
-            const int c = (2 * ks + hi) ^ (rsw & 15);
-            s = mfma32x32x16(as_bf16x8(lq[stg][rsw * 16 + c]), kf[ks], s);
-            const bf16x8 vf = as_bf16x8(lvk[vr_ * 16 + ((2 * ks + hi) ^ (vr_ & 15))]);
-            dp = mfma32x32x16(as_bf16x8(ldo_[stg][rsw * 16 + c]), vf, dp);
-        }
-        // Register i holds query qb0 + 16 (i / 8) + 8 hi + i % 8.
-        bf16x8 pa[2], da[2];
+        for (int rb = 0; rb < 2; ++rb) {
+            if (qb0 + 32 * rb + 31 < k0w) continue;   // every query of the half precedes the wave's keys
+            f32x16 s = f32x16{}, dp = f32x16{};
+            const int row = 32 * rb + rsw;
 #pragma unroll
-        for (int h = 0; h < 2; ++h) {
-            const int qo = 16 * h + 8 * hi;
-            // Branch-free: the exponent is computed for every entry (masked ones may be
-            // garbage) and the mask selects 0; the 8 statistics are two 16-byte reads each.
-            const f32x4 l0 = *(const f32x4*)&lstat[stg][qo], l1 = *(const f32x4*)&lstat[stg][qo + 4];
-            const f32x4 d0 = *(const f32x4*)&lstat[stg][KV_BQ + qo], d1 = *(const f32x4*)&lstat[stg][KV_BQ + qo + 4];
-            float pe[8], de[8];
-#pragma unroll
-            for (int k = 0; k < 8; ++k) {
-                const int qi = qb0 + qo + k;
-                const float lse = k < 4 ? l0[k] : l1[k - 4], dd = k < 4 ? d0[k] : d1[k - 4];
-                const bool vis = key <= qi && qi < A.S;
-                const float e = __builtin_amdgcn_exp2f(fmaf(s[8 * h + k], A.scale_log2, -lse));
-                pe[k] = vis ? e : 0.f;
-                de[k] = vis ? e * (dp[8 * h + k] - dd) : 0.f;
+            for (int ks = 0; ks < 8; ++ks) {
+                s = mfma32x32x16(row8<KV_BQ>(lq[stg], row, 16 * ks + 8 * hi), kf[ks], s);
+                dp = mfma32x32x16(row8<KV_BQ>(ldo_[stg], row, 16 * ks + 8 * hi),
+                                  tr_frag<D, false>(lvt, 16 * ks, 32 * wave, lane), dp);
             }
-            pa[h] = pack8(pe);
-            da[h] = pack8(de);
-        }
+            // Register i holds query qb0 + 32 rb + 16 (i / 8) + 8 hi + i % 8.
+            bf16x8 pa[2], da[2];
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
+            for (int h = 0; h < 2; ++h) {
+                const int qo = 32 * rb + 16 * h + 8 * hi;
+                // Branch-free: the exponent is computed for every entry (masked ones may be
+                // garbage) and the mask selects 0; the 8 statistics are two 16-byte reads each.
+                const f32x4 l0 = *(const f32x4*)&lstat[stg][qo], l1 = *(const f32x4*)&lstat[stg][qo + 4];
+                const f32x4 d0 = *(const f32x4*)&lstat[stg][KV_BQ + qo];
+                const f32x4 d1 = *(const f32x4*)&lstat[stg][KV_BQ + qo + 4];
+                float pe[8], de[8];
 #pragma unroll
-            for (int nb = 0; nb < 4; ++nb) {
-                const int d = 32 * nb + l32;
-                const int ch = (2 * h + hi) ^ ((d >> 2) & 3);
-                dv[nb] = mfma32x32x16(pa[h], as_bf16x8(ldot[stg][d * 4 + ch]), dv[nb]);
-                dk[nb] = mfma32x32x16(da[h], as_bf16x8(lqt[stg][d * 4 + ch]), dk[nb]);
+                for (int k = 0; k < 8; ++k) {
+                    const int qi = qb0 + qo + k;
+                    const float lse = k < 4 ? l0[k] : l1[k - 4], dd = k < 4 ? d0[k] : d1[k - 4];
+                    const bool vis = key <= qi && qi < A.S;
+                    const float e = __builtin_amdgcn_exp2f(fmaf(s[8 * h + k], A.scale_log2, -lse));
+                    pe[k] = vis ? e : 0.f;
+                    de[k] = vis ? e * (dp[8 * h + k] - dd) : 0.f;
+                }
+                pa[h] = pack8(pe);
+                da[h] = pack8(de);
             }
+#pragma unroll
+            for (int h = 0; h < 2; ++h)
+#pragma unroll
+                for (int nb = 0; nb < 4; ++nb) {
+                    dv[nb] = mfma32x32x16(pa[h], tr_frag<KV_BQ, false>(ldo_[stg], 32 * rb + 16 * h, 32 * nb, lane), dv[nb]);
+                    dk[nb] = mfma32x32x16(da[h], tr_frag<KV_BQ, false>(lq[stg], 32 * rb + 16 * h, 32 * nb, lane), dk[nb]);
+                }
+        }
     }
 
     // Epilogue: lane column d = 32 nb + l32; register e of block nb holds key
@@ -392,13 +420,14 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) yk[nb] = yv[nb] = 0.f;
         }
-        if (A.outT && kk < A.Sp) {
-            const size_t col = (size_t)b * A.Sp + kk;
-            const size_t ldt2 = (size_t)A.B * A.Sp;
+        // Transposed copy, column = token b * S + kk; the last sequence also writes the zero
+        // tail up to Mp.
+        const size_t col = (size_t)b * A.S + kk;
+        if (A.outT && (kk < A.S || (b == A.B - 1 && col < (size_t)A.Mp))) {
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) {
-                A.outT[(size_t)(A.col_k + kvh * D + 32 * nb + l32) * ldt2 + col] = f2bf(yk[nb]);
-                A.outT[(size_t)(A.col_v + kvh * D + 32 * nb + l32) * ldt2 + col] = f2bf(yv[nb]);
+                A.outT[(size_t)(A.col_k + kvh * D + 32 * nb + l32) * A.Mp + col] = f2bf(yk[nb]);
+                A.outT[(size_t)(A.col_v + kvh * D + 32 * nb + l32) * A.Mp + col] = f2bf(yv[nb]);
             }
         }
     }
@@ -406,12 +435,12 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
 
 // ---------------------------------------------------------------------------
 // dQ.  Workgroup = 8 waves = 256 queries of one (sequence, head); wave w owns queries
-// 32 w .. 32 w + 31 (lane: one query column).  Key blocks of 64 stream through LDS as
-// K and V rows ([64][128], 256-byte rows) and K^T ([128][64], 128-byte rows), double
-// buffered (2 x 48 KB).
+// 32 w .. 32 w + 31 (lane: one query column).  Key blocks of 128 stream through LDS as
+// K rows and V^T rows straight from the producer's slot ([128][128] each, sub-tiled
+// layout), double buffered (2 x 64 KB).  Each 64-key half:
 //   S^T  [32 k x 32 q] x 2 = K Q^T      (A = K rows, permuted; B = Q, registers)
-//   dP^T [32 k x 32 q] x 2 = V dO^T     (A = V rows, same order; B = dO, registers)
-//   dQ^T [128 x 32 q]     += K^T dS^T   (A = K^T from LDS; B = dS^T from the registers)
+//   dP^T [32 k x 32 q] x 2 = V dO^T     (A = V^T tile along its rows, same order; B = dO)
+//   dQ^T [128 x 32 q]     += K^T dS^T   (A = K tile along its rows; B = dS^T, registers)
 // ---------------------------------------------------------------------------
 struct QArgs {
     const uint16_t* q;      // [B*S][a*128]
@@ -419,22 +448,20 @@ struct QArgs {
     const float* lse;       // [B][a][Sp]
     const float* dsum;      // [B][a][Sp]
     const uint16_t* kc;     // producer K slot [Bmax][g][cap][128]
-    const uint16_t* kt;     // K^T [B*g][128][Sp], zero past S
-    const uint16_t* vr;     // V rows [B*g][Sp][128], zero past S
+    const uint16_t* vc;     // producer V slot [Bmax][g][128][cap]
     const float2* rope;     // [S][64]
     uint16_t* out;          // dQ rows [B*S][ldo] at column head*128, or null
-    uint16_t* outT;         // dQ^T [a*128][B*Sp] (rows head*128 + d), or null
+    uint16_t* outT;         // dQ^T [a*128][Mp] (rows head*128 + d, column = token), or null
     int ldo;
-    int B, S, Sp, a, g, cap;
+    int B, S, Sp, Mp, a, g, cap;
     float scale_log2, scale;
 };
 
-constexpr int Q_BQ = 256, Q_BKV = 64, Q_NT = 512;
+constexpr int Q_BQ = 256, Q_BKV = 128, Q_NT = 512;
 
 __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
     __shared__ u32x4 lk[2][Q_BKV * 16];
-    __shared__ u32x4 lv[2][Q_BKV * 16];
-    __shared__ u32x4 lkt[2][D * 8];
+    __shared__ u32x4 lvt[2][D * 16];
 
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int l32 = lane & 31, hi = lane >> 5;
@@ -462,25 +489,23 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
 
     const size_t plane = (size_t)b * A.g + kvh;
     const uint16_t* kbase = A.kc + plane * A.cap * D;
-    const uint16_t* vbase = A.vr + plane * A.Sp * D;
-    const uint16_t* tbase = A.kt + plane * D * A.Sp;
+    const uint16_t* vbase = A.vc + plane * D * A.cap;
     const int last_q = min(qt * Q_BQ + Q_BQ - 1, A.S - 1);
     const int ntiles = last_q / Q_BKV + 1;
 
+    // K rows past S are replaced by row S - 1 (finite: they meet dS = 0 in dQ); V^T chunks
+    // past the slot are clamped (their keys' dP rows are masked).
+    const int ch = sub_chunk(lane);
     auto issue = [&](int t, int stg) {
         const int t0 = t * Q_BKV;
 #pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int row = 8 * wave + 4 * j + (lane >> 4);
-            const int c = (lane & 15) ^ (row & 15);
-            load_lds16(kbase + (size_t)(t0 + row) * D + 8 * c, &lk[stg][(8 * wave + 4 * j) * 16]);
-            load_lds16(vbase + (size_t)(t0 + row) * D + 8 * c, &lv[stg][(8 * wave + 4 * j) * 16]);
-        }
-#pragma unroll
-        for (int j = 0; j < 2; ++j) {
-            const int d = 16 * wave + 8 * j + (lane >> 3);
-            const int c = (lane & 7) ^ ((d >> 1) & 7);
-            load_lds16(tbase + (size_t)d * A.Sp + t0 + 8 * c, &lkt[stg][(16 * wave + 8 * j) * 8]);
+        for (int j = 0; j < 4; ++j) {
+            const int u = 4 * wave + j, sb = u >> 3, q = u & 7;
+            const int row = 16 * q + (lane >> 2);
+            load_lds16(kbase + (size_t)min(t0 + row, A.S - 1) * D + 32 * sb + 8 * ch,
+                       (char*)lk[stg] + sb * (Q_BKV * 64) + q * 1024);
+            load_lds16(vbase + (size_t)row * A.cap + min(t0 + 32 * sb + 8 * ch, A.cap - 8),
+                       (char*)lvt[stg] + sb * (D * 64) + q * 1024);
         }
     };
 
@@ -496,51 +521,55 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
         __syncthreads();
         if (t + 1 < ntiles) issue(t + 1, stg ^ 1);
         const int t0 = t * Q_BKV;
-        if (t0 > q0w + 31 || q0w >= A.S) continue;    // no key of the block is visible to the wave
-        f32x16 s[2], dp[2];
+        if (q0w >= A.S) continue;
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb) {
-            s[mb] = f32x16{};
-            dp[mb] = f32x16{};
-            const int row = 32 * mb + rsw;
+        for (int hf = 0; hf < 2; ++hf) {
+            const int k0 = 64 * hf;                         // first key of the half in the tile
+            if (t0 + k0 > q0w + 31) continue;              // no key of the half is visible
+            f32x16 s[2], dp[2];
 #pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
-                const int c = (2 * ks + hi) ^ (row & 15);
-                s[mb] = mfma32x32x16(as_bf16x8(lk[stg][row * 16 + c]), qf[ks], s[mb]);
-                dp[mb] = mfma32x32x16(as_bf16x8(lv[stg][row * 16 + c]), df[ks], dp[mb]);
-            }
-        }
-        // Register i of block mb holds key t0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
-        bf16x8 db_[4];
+            for (int mb = 0; mb < 2; ++mb) {
+                s[mb] = f32x16{};
+                dp[mb] = f32x16{};
+                const int row = k0 + 32 * mb + rsw;
 #pragma unroll
-        for (int mb = 0; mb < 2; ++mb)
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                float de[8];
-#pragma unroll
-                for (int k = 0; k < 8; ++k) {
-                    const int kk = t0 + 32 * mb + 16 * h + 8 * hi + k;
-                    const bool vis = kk <= ql && ql < A.S;
-                    const float e = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + k], A.scale_log2, -lse));
-                    de[k] = vis ? e * (dp[mb][8 * h + k] - dd) : 0.f;
+                for (int ks = 0; ks < 8; ++ks) {
+                    s[mb] = mfma32x32x16(row8<Q_BKV>(lk[stg], row, 16 * ks + 8 * hi), qf[ks], s[mb]);
+                    dp[mb] = mfma32x32x16(tr_frag<D, true>(lvt[stg], 16 * ks, k0 + 32 * mb, lane), df[ks], dp[mb]);
                 }
-                db_[2 * mb + h] = pack8(de);
             }
+            // Register i of block mb holds key t0 + k0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
+            bf16x8 db_[4];
 #pragma unroll
-        for (int c = 0; c < 4; ++c)
+            for (int mb = 0; mb < 2; ++mb)
 #pragma unroll
-            for (int m = 0; m < 4; ++m) {
-                const int d = 32 * m + l32;
-                const int ch = (2 * c + hi) ^ ((d >> 1) & 7);
-                dq[m] = mfma32x32x16(as_bf16x8(lkt[stg][d * 8 + ch]), db_[c], dq[m]);
-            }
+                for (int h = 0; h < 2; ++h) {
+                    float de[8];
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int kk = t0 + k0 + 32 * mb + 16 * h + 8 * hi + k;
+                        const bool vis = kk <= ql && ql < A.S;
+                        const float e = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + k], A.scale_log2, -lse));
+                        de[k] = vis ? e * (dp[mb][8 * h + k] - dd) : 0.f;
+                    }
+                    db_[2 * mb + h] = pack8(de);
+                }
+#pragma unroll
+            for (int c = 0; c < 4; ++c)
+#pragma unroll
+                for (int m = 0; m < 4; ++m)
+                    dq[m] = mfma32x32x16(tr_frag<Q_BKV, false>(lk[stg], k0 + 16 * c, 32 * m, lane), db_[c], dq[m]);
+        }
     }
 
     // Epilogue: lane column = query ql; register e of block m holds dim
-    // 32 m + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate back (pairs m, m + 2), write.
-    if (ql < A.Sp) {
-        const bool valid = ql < A.S;
-        const size_t col = (size_t)b * A.Sp + ql, ldt = (size_t)A.B * A.Sp;
+    // 32 m + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate back (pairs m, m + 2), write rows
+    // and the transposed copy (column = token b * S + ql; the last sequence also writes
+    // the zero tail up to Mp).
+    const bool valid = ql < A.S;
+    const size_t col = (size_t)b * A.S + ql;
+    const bool tcol = valid || (b == A.B - 1 && col < (size_t)A.Mp);
+    if (valid || tcol) {
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             float y[4][4];   // [block m][e % 4]
@@ -564,10 +593,10 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
                     w[1] = pack2bf(y[m][2], y[m][3]);
                     *(u32x2*)(A.out + ((size_t)b * A.S + ql) * A.ldo + head * D + d0) = w;
                 }
-                if (A.outT) {
+                if (A.outT && tcol) {
 #pragma unroll
                     for (int e4 = 0; e4 < 4; ++e4)
-                        A.outT[(size_t)(head * D + d0 + e4) * ldt + col] = f2bf(y[m][e4]);
+                        A.outT[(size_t)(head * D + d0 + e4) * A.Mp + col] = f2bf(y[m][e4]);
                 }
             }
         }
@@ -603,21 +632,19 @@ hipError_t reduce_planes(const float* part, int planes, int M, int N, float* dst
     return hipGetLastError();
 }
 
-hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, const uint16_t* Q, float* dsum,
-                              uint16_t* dOt, uint16_t* Qt, uint16_t* Ot, int B, int S, int Sp, int a,
-                              hipStream_t st) {
-    hipLaunchKernelGGL(attn_bwd_prep_kernel, dim3(B * a * (Sp / 64)), dim3(256), 0, st, dO, O, Q, dsum,
-                       dOt, Qt, Ot, B, S, Sp, a);
+hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, float* dsum, uint16_t* Ot, int B,
+                              int S, int Sp, int Mp, int a, hipStream_t st) {
+    hipLaunchKernelGGL(attn_bwd_prep_kernel, dim3((Mp / 64) * a), dim3(256), 0, st, dO, O, dsum, Ot, B, S,
+                       Sp, Mp, a);
     return hipGetLastError();
 }
 
 hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
     KvArgs A;
-    A.q = p.q; A.qt = p.qt; A.dO = p.dO; A.dOt = p.dOt; A.lse = p.lse; A.dsum = p.dsum;
-    A.kc = p.kc; A.vr = p.vr; A.rope = p.rope;
+    A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.vc = p.vc; A.rope = p.rope;
     A.acc_in_k = p.acc_in_k; A.acc_in_v = p.acc_in_v; A.acc_out_k = p.acc_out_k; A.acc_out_v = p.acc_out_v;
     A.out = p.out; A.outT = p.outT; A.ldo = p.ldo; A.col_k = p.col_k; A.col_v = p.col_v;
-    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
+    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.Mp = p.Mp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int nkb = (p.S + KV_BK - 1) / KV_BK;
@@ -627,9 +654,9 @@ hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
 
 hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st) {
     QArgs A;
-    A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.kt = p.kt; A.vr = p.vr;
+    A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.vc = p.vc;
     A.rope = p.rope; A.out = p.out; A.outT = p.outT; A.ldo = p.ldo;
-    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
+    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.Mp = p.Mp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int nqt = (p.S + Q_BQ - 1) / Q_BQ;

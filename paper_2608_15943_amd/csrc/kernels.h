@@ -58,20 +58,19 @@ hipError_t f32_to_bf16(const float* x, uint16_t* y, size_t n, hipStream_t st);
 // Sum of `planes` [M][N] fp32 planes; rows [0, rows0) -> dst0, then rows1 -> dst1, rest -> dst2.
 hipError_t reduce_planes(const float* part, int planes, int M, int N, float* dst0, int rows0, float* dst1,
                          int rows1, float* dst2, hipStream_t st);
-// D = rowsum(dO * O) [B][a][Sp] and dO^T, Q^T, O^T [a*128][B*Sp] (zero past S).
-hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, const uint16_t* Q, float* dsum,
-                              uint16_t* dOt, uint16_t* Qt, uint16_t* Ot, int B, int S, int Sp, int a,
-                              hipStream_t st);
+// D = rowsum(dO * O) [B][a][Sp] and O^T [a*128][Mp] (column = token, zero tail).
+hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, float* dsum, uint16_t* Ot, int B,
+                              int S, int Sp, int Mp, int a, hipStream_t st);
 
+// Transposed outputs (outT) are [rows][Mp] with column = token b * S + s, Mp = B * S
+// rounded up to 64, zero tail.
 struct AttnBwdKv {
-    const uint16_t* q;
-    const uint16_t* qt;
-    const uint16_t* dO;
-    const uint16_t* dOt;
-    const float* lse;
-    const float* dsum;
+    const uint16_t* q;      // post-RoPE Q of the layer [B*S][a*128]
+    const uint16_t* dO;     // [B*S][a*128]
+    const float* lse;       // [B][a][Sp]
+    const float* dsum;      // [B][a][Sp]
     const uint16_t* kc;     // producer K slot
-    const uint16_t* vr;     // producer V rows [B*g][Sp][128], zero past S
+    const uint16_t* vc;     // producer V slot (transposed)
     const float2* rope;
     const float* acc_in_k;
     const float* acc_in_v;
@@ -80,7 +79,7 @@ struct AttnBwdKv {
     uint16_t* out;
     uint16_t* outT;
     int ldo, col_k, col_v;
-    int B, S, Sp, a, g, cap;
+    int B, S, Sp, Mp, a, g, cap;
 };
 hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st);
 
@@ -90,13 +89,12 @@ struct AttnBwdQ {
     const float* lse;
     const float* dsum;
     const uint16_t* kc;
-    const uint16_t* kt;
-    const uint16_t* vr;
+    const uint16_t* vc;
     const float2* rope;
     uint16_t* out;
     uint16_t* outT;
     int ldo;
-    int B, S, Sp, a, g, cap;
+    int B, S, Sp, Mp, a, g, cap;
 };
 hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st);
 

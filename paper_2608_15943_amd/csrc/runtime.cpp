@@ -540,10 +540,11 @@ Saved saved_layout(const kvp_ctx& c, int B, int S) {
     return v;
 }
 
-// Workspace of kvp_backward.
+// Workspace of kvp_backward.  Transposed activations are [rows][Mp], column = token
+// (Mp = B * S rounded up to 64, zero tail).
 struct BwdWs {
-    size_t gb = 0, gbt = 0, dO = 0, dOt = 0, qt = 0, ot = 0, xt = 0, dsum = 0, dqkv = 0, dqkvt = 0;
-    size_t kt = 0, vr = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
+    size_t gb = 0, gbt = 0, dO = 0, ot = 0, xt = 0, dsum = 0, dqkv = 0, dqkvt = 0;
+    size_t acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
     size_t acc_plane = 0;          // floats of one dK or dV sum
     std::vector<int> acc_slot;     // per layer: index of its fp32 sum pair, or -1
 };
@@ -556,20 +557,16 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
         off += align_up(bytes);
         return at;
     };
-    const size_t M = (size_t)B * S, Sp = round64(S), T = (size_t)B * Sp;
+    const size_t M = (size_t)B * S, Mp = round64((int)M);
     const size_t h = c.d.h, nq = c.n_q(), nkv = c.n_kv(), np = nq + 2 * nkv;
     w.gb = take(M * h * 2);
-    w.gbt = take(h * T * 2);
+    w.gbt = take(h * Mp * 2);
     w.dO = take(M * nq * 2);
-    w.dOt = take(nq * T * 2);
-    w.qt = take(nq * T * 2);
-    w.ot = take(nq * T * 2);
-    w.xt = take(h * T * 2);
-    w.dsum = take((size_t)B * c.d.a * Sp * sizeof(float));
+    w.ot = take(nq * Mp * 2);
+    w.xt = take(h * Mp * 2);
+    w.dsum = take((size_t)B * c.d.a * round64(S) * sizeof(float));
     w.dqkv = take(M * np * 2);
-    w.dqkvt = take(np * T * 2);
-    w.kt = take((size_t)B * c.d.g * 128 * Sp * 2);
-    w.vr = take((size_t)B * c.d.g * Sp * 128 * 2);
+    w.dqkvt = take(np * Mp * 2);
     // One fp32 dK/dV pair per producer that has consumers.
     w.acc_slot.assign(c.d.L, -1);
     int nacc = 0;
@@ -585,9 +582,9 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
     w.wot = take(nq * h * 2);
     w.wst = take(h * np * 2);
     // Split-K partial planes of the weight-gradient GEMMs (consumers: Q rows only).
-    const int so = kvp::gemm_out_splits((int)h, (int)nq, (int)T);
-    const int sp = kvp::gemm_out_splits((int)np, (int)h, (int)T);
-    const int sc = kvp::gemm_out_splits((int)nq, (int)h, (int)T);
+    const int so = kvp::gemm_out_splits((int)h, (int)nq, (int)Mp);
+    const int sp = kvp::gemm_out_splits((int)np, (int)h, (int)Mp);
+    const int sc = kvp::gemm_out_splits((int)nq, (int)h, (int)Mp);
     w.part = take(std::max({(size_t)so * h * nq, (size_t)sp * np * h, (size_t)sc * nq * h}) * sizeof(float));
     w.rope = take((size_t)S * 64 * sizeof(float2));
     w.total = off;
@@ -790,8 +787,8 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
     if (B > ctx->d.max_batch || S > ctx->d.max_seq)
         return fail(KVP_E_CAPACITY, "kvp_backward: B=%d, S=%d exceed max_batch / max_seq", B, S);
     const int h = ctx->d.h, nq = ctx->n_q(), nkv = ctx->n_kv(), L = ctx->d.L;
-    const int Sp = round64(S), M = B * S, T = B * Sp;
-    if ((int64_t)(nq + 2 * nkv) * T > INT32_MAX || (int64_t)M * std::max(h, nq + 2 * nkv) > INT32_MAX)
+    const int Sp = round64(S), M = B * S, Mp = round64(M);
+    if ((int64_t)(nq + 2 * nkv) * Mp > INT32_MAX || (int64_t)M * std::max(h, nq + 2 * nkv) > INT32_MAX)
         return fail(KVP_E_SHAPE, "kvp_backward: sizes exceed the 32-bit index range");
     const Saved sv = saved_layout(*ctx, B, S);
     if (!saved || saved_bytes < sv.total || !aligned16(saved))
@@ -811,14 +808,12 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
     char* base = (char*)ws;
     const char* sb = (const char*)saved;
     auto bp = [&](size_t off) { return (uint16_t*)(base + off); };
-    uint16_t *gb = bp(w.gb), *gbt = bp(w.gbt), *dO = bp(w.dO), *dOt = bp(w.dOt), *qt = bp(w.qt),
-             *ot = bp(w.ot), *xt = bp(w.xt), *dqkv = bp(w.dqkv), *dqkvt = bp(w.dqkvt), *kt = bp(w.kt),
-             *vr = bp(w.vr), *wot = bp(w.wot), *wst = bp(w.wst);
+    uint16_t *gb = bp(w.gb), *gbt = bp(w.gbt), *dO = bp(w.dO), *ot = bp(w.ot), *xt = bp(w.xt),
+             *dqkv = bp(w.dqkv), *dqkvt = bp(w.dqkvt), *wot = bp(w.wot), *wst = bp(w.wst);
     float* dsum = (float*)(base + w.dsum);
     float* acc = (float*)(base + w.acc);
     float* part = (float*)(base + w.part);
     const float2* rope = (const float2*)(base + w.rope);
-    const size_t tld = (size_t)T;
     auto aux = [&](auto&& f) { return timed(ctx, KVP_K_BWD_AUX, st, f); };
     auto gemm = [&](auto&& f) { return timed(ctx, KVP_K_BWD_GEMM, st, f); };
 
@@ -830,7 +825,6 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         return rc;
 
     std::vector<char> acc_written(L, 0);
-    int kt_owner = -1;
     for (int l = L - 1; l >= 0; --l) {
         const int p = ctx->tau[l];
         const bool producer = p == l;
@@ -852,46 +846,29 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gb, wot, M, nq, h, 1, dO, true, st), "dO GEMM"); })))
             return rc;
         if ((rc = aux([&] {
-                 return check_hip(kvp::attn_bwd_prep_bf16(dO, Ol, Ql, dsum, dOt, qt, ot, B, S, Sp, ctx->d.a, st),
+                 return check_hip(kvp::attn_bwd_prep_bf16(dO, Ol, dsum, ot, B, S, Sp, Mp, ctx->d.a, st),
                                   "attention backward prep");
              })))
             return rc;
         // dW_O = G^T O.
         if ((rc = aux([&] {
-                 return check_hip(kvp::transpose_bf16(gb, gbt, B, S, h, h, (size_t)S * h, tld, Sp, Sp, h, st),
-                                  "transpose G");
+                 return check_hip(kvp::transpose_bf16(gb, gbt, 1, M, h, h, 0, Mp, 0, Mp, h, st), "transpose G");
              })))
             return rc;
         {
-            const int s = kvp::gemm_out_splits(h, nq, T);
-            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gbt, ot, h, nq, T, s, part, false, st), "dW_O GEMM"); })))
+            const int s = kvp::gemm_out_splits(h, nq, Mp);
+            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gbt, ot, h, nq, Mp, s, part, false, st), "dW_O GEMM"); })))
                 return rc;
             if ((rc = aux([&] {
                      return check_hip(kvp::reduce_planes(part, s, h, nq, Ly.dwo, h, nullptr, 0, nullptr, st), "dW_O sum");
                  })))
                 return rc;
         }
-        // The producer's K^T and V rows for the dQ kernel.
-        if (kt_owner != p) {
-            const int planes = B * ctx->d.g, cap = ctx->d.kv_capacity;
-            if ((rc = aux([&] {
-                     int r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Pl.kc, kt, planes, S, 128, 128,
-                                                            (size_t)cap * 128, Sp, (size_t)128 * Sp, Sp, 128, st),
-                                        "transpose K");
-                     if (!r2)
-                         r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Pl.vc, vr, planes, 128, S, cap,
-                                                            (size_t)128 * cap, 128, (size_t)Sp * 128, 128, Sp, st),
-                                        "transpose V");
-                     return r2;
-                 })))
-                return rc;
-            kt_owner = p;
-        }
         // dK, dV: a consumer adds into its producer's fp32 sums; the producer finishes them.
         {
             kvp::AttnBwdKv a{};
-            a.q = Ql; a.qt = qt; a.dO = dO; a.dOt = dOt; a.lse = lse; a.dsum = dsum;
-            a.kc = (const uint16_t*)Pl.kc; a.vr = vr; a.rope = rope;
+            a.q = Ql; a.dO = dO; a.lse = lse; a.dsum = dsum;
+            a.kc = (const uint16_t*)Pl.kc; a.vc = (const uint16_t*)Pl.vc; a.rope = rope;
             const int slot = w.acc_slot[p];
             float* ak = slot >= 0 ? acc + (size_t)slot * 2 * w.acc_plane : nullptr;
             float* av = slot >= 0 ? ak + w.acc_plane : nullptr;
@@ -910,7 +887,7 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
                 a.col_k = nq;
                 a.col_v = nq + nkv;
             }
-            a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
+            a.B = B; a.S = S; a.Sp = Sp; a.Mp = Mp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
             if ((rc = timed(ctx, KVP_K_BWD_ATTN_KV, st, [&] {
                      return check_hip(kvp::flash_bwd_kv_bf16(a, st), "attention backward dK dV");
                  })))
@@ -918,9 +895,9 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         }
         {
             kvp::AttnBwdQ a{};
-            a.q = Ql; a.dO = dO; a.lse = lse; a.dsum = dsum; a.kc = (const uint16_t*)Pl.kc; a.kt = kt;
-            a.vr = vr; a.rope = rope; a.out = dqkv; a.outT = dqkvt; a.ldo = np;
-            a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
+            a.q = Ql; a.dO = dO; a.lse = lse; a.dsum = dsum; a.kc = (const uint16_t*)Pl.kc;
+            a.vc = (const uint16_t*)Pl.vc; a.rope = rope; a.out = dqkv; a.outT = dqkvt; a.ldo = np;
+            a.B = B; a.S = S; a.Sp = Sp; a.Mp = Mp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
             if ((rc = timed(ctx, KVP_K_BWD_ATTN_Q, st, [&] {
                      return check_hip(kvp::flash_bwd_q_bf16(a, st), "attention backward dQ");
                  })))
@@ -928,13 +905,12 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         }
         // dW_Q (| dW_K | dW_V) = [dQ | dK | dV]^T X_l.
         if ((rc = aux([&] {
-                 return check_hip(kvp::transpose_bf16(Xl, xt, B, S, h, h, (size_t)S * h, tld, Sp, Sp, h, st),
-                                  "transpose X");
+                 return check_hip(kvp::transpose_bf16(Xl, xt, 1, M, h, h, 0, Mp, 0, Mp, h, st), "transpose X");
              })))
             return rc;
         {
-            const int s = kvp::gemm_out_splits(np, h, T);
-            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(dqkvt, xt, np, h, T, s, part, false, st), "dW_QKV GEMM"); })))
+            const int s = kvp::gemm_out_splits(np, h, Mp);
+            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(dqkvt, xt, np, h, Mp, s, part, false, st), "dW_QKV GEMM"); })))
                 return rc;
             if ((rc = aux([&] {
                      return check_hip(kvp::reduce_planes(part, s, np, h, Ly.dwq, nq, Ly.dwk, producer ? nkv : 0,
