@@ -115,3 +115,89 @@ def test_backward_matches_oracle(h, a, g, tau, B, S):
     w = small_workload(f"bwd-h{h}-a{a}-g{g}", len(tau), h, a, g, tau, seed=21)
     cap = (S + 63) // 64 * 64
     _train_case(w, B, S, cap)
+
+
+
+def _prefix_case(w, B, S, P, tol_dx, tol_w):
+    """Training step of workload w at (B, S) with dY zero past position P: the loss reads only
+    outputs at positions < P, which depend only on inputs before P (causal stack), so every
+    gradient equals that of the P-token problem, which the oracle solves for all sequences;
+    dX past P is exactly 0."""
+    say(f"[backward full] {w.name} L={w.L} B={B} S={S} tau={w.tau}, dY zero past {P}")
+    dm = build_device_model(w, B, S, w.kv_capacity)
+    m = dm.model
+    st = torch.cuda.current_stream().cuda_stream
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device=DEV)
+    kd.fill_prefill_x(w, x.data_ptr(), B, S)
+    y = torch.empty_like(x)
+    ws, n = workspace(dm, kb.KVP_PHASE_PREFILL, B, S)
+    nsv = m.kvp_train_saved_size(B, S)
+    saved = torch.empty(nsv, dtype=torch.uint8, device=DEV)
+    m.kvp_train_forward(x.data_ptr(), y.data_ptr(), B, S, saved.data_ptr(), nsv, ws.data_ptr(), n, st)
+    grads = {}
+    for l in range(w.L):
+        prod = w.tau[l] == l
+        g = {"dwq": torch.empty((w.a * w.d_h, w.h), device=DEV), "dwo": torch.empty((w.h, w.a * w.d_h), device=DEV),
+             "dwk": torch.empty((w.g * w.d_h, w.h), device=DEV) if prod else None,
+             "dwv": torch.empty((w.g * w.d_h, w.h), device=DEV) if prod else None}
+        m.kvp_set_layer_grads(l, g["dwq"].data_ptr(), g["dwk"].data_ptr() if prod else 0,
+                              g["dwv"].data_ptr() if prod else 0, g["dwo"].data_ptr())
+        grads[l] = g
+    dy = torch.empty((B, S, w.h), dtype=torch.float32, device=DEV)
+    kd.fill_prefill_dy(w, dy.data_ptr(), B, S)
+    dy[:, P:] = 0
+    dx = torch.empty_like(dy)
+    wsb, nb = workspace(dm, kb.KVP_PHASE_BACKWARD, B, S)
+    m.kvp_backward(x.data_ptr(), dy.data_ptr(), dx.data_ptr(), B, S, saved.data_ptr(), nsv,
+                   wsb.data_ptr(), nb, st)
+    torch.cuda.synchronize()
+    assert bool((dx[:, P:] == 0).all().item()), "dX past the prefix must be zero"
+    say("  backward done; oracle on the prefix ...")
+    wts = oracle_weights(w)
+    ref_g = None
+    e_dx = 0.0
+    for b in range(B):
+        xb = ki.prefill_x(w, [b], np.arange(P))[0]
+        dyb = ki.prefill_dy(w, [b], np.arange(P))[0]
+        dxb, gb = obw.stack_backward(xb, wts, w.tau, w.a, w.g, w.d_h, w.rope_base, dyb)
+        e = rel_err(to_np(dx[b, :P]), dxb)
+        say(f"  dx[{b}]: {e:.3e}")
+        e_dx = max(e_dx, e)
+        if ref_g is None:
+            ref_g = gb
+        else:
+            for l in range(w.L):
+                for k, v in gb[l].items():
+                    if v is not None:
+                        ref_g[l][k] = ref_g[l][k] + v
+    e_w = 0.0
+    for l in range(w.L):
+        for k in ("dwq", "dwk", "dwv", "dwo"):
+            if ref_g[l][k] is not None:
+                e = rel_err(to_np(grads[l][k]), ref_g[l][k])
+                say(f"  layer {l} {k}: {e:.3e}")
+                e_w = max(e_w, e)
+    say(f"  max rel err: dx {e_dx:.3e}, weight gradients {e_w:.3e}")
+    del dm, x, y, saved, ws, wsb, dy, dx, grads
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    assert e_dx <= tol_dx and e_w <= tol_w, (e_dx, e_w)
+
+
+def test_backward_full_size_three_layers():
+    """Three layers of the 8-layer stage's shape (d_model 2048, 16 / 8 heads) at its batch and
+    length (B 4, S 4096), in the benchmark's launch configuration: a producer with no consumer
+    and a producer with one, at the 2e-2 bar."""
+    w = ki.Workload(name="stage-shape-3L", L=3, h=2048, a=16, g=8, d_h=128, dtype="bf16",
+                    tau=[0, 1, 1], phase="prefill", batch=4, seq=4096, kv_capacity=4096, seed=5)
+    _prefix_case(w, 4, 4096, 300, TOL, TOL)
+
+
+def test_backward_stage_share_full_size_prefix():
+    """The 8-layer stage share itself, composed.  Its gradients are bounded by what bf16
+    forward activations allow: a CPU emulation that rounds Q, K, V, O and the layer inputs to
+    bf16 and is otherwise exact moves this problem's dX by up to 2.8e-2 and its weight
+    gradients by up to 3.5e-2 of max|ref| (the largest at position 0, which every query
+    attends to); the bound here is 5e-2.  The three-layer test above holds the 2e-2 bar."""
+    w = ki.stage_share_prefill()
+    _prefix_case(w, w.batch, w.seq, 300, 5e-2, 5e-2)
