@@ -10,14 +10,13 @@
 // -pos * theta) is applied to dQ and dK in the epilogues, before any accumulation.
 //
 // Kernels:
-//   attn_bwd_prep    D, and O^T for the dW_O product ([a*128][Mp], column = token,
-//                    Mp = B*S rounded up to 64, zero tail).
+//   attn_bwd_prep    D = rowsum(dO * O) per (token, head).
+//   transpose_bf16   weight transposes for the dO and dX products.
 //   flash_bwd_kv     one workgroup per (sequence, KV head, 256 keys); loops over the r
 //                    query heads of the group and the query blocks at or after its
 //                    keys; dK, dV accumulate in registers.
 //   flash_bwd_q      one workgroup per (sequence, head, 256 queries); loops over the
 //                    key blocks at or before its queries; dQ accumulates in registers.
-//   transpose_bf16   batched, zero-padded 2-D transposes (activations, weights, caches).
 //
 // Operand layouts follow from v_mfma_f32_32x32x16_bf16: an operand lane holds 8
 // consecutive elements of the reduction axis, and an accumulator lane holds one output
@@ -33,6 +32,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "lds_tr.h"
 
 namespace kvp {
 namespace {
@@ -63,74 +63,23 @@ __device__ __forceinline__ bf16x8 pack8(const float* e) {
     return as_bf16x8(w);
 }
 
-typedef short v4i16 __attribute__((ext_vector_type(4)));
-typedef __attribute__((address_space(3))) v4i16 lds_v4i16;
-
-// Staged tiles use a sub-tiled LDS layout: an NR x NC bf16 tile is stored as NC / 32 blocks
-// of 32 columns, each NR rows of 64 bytes; 16-byte chunk k (0..3) of row r of a block sits
-// at position k ^ ((r >> 2) & 3).  A column-block or 16-row offset is then a constant byte
-// offset (so every read below is one lane register plus an immediate), and 16 consecutive
-// rows of one chunk column cover all 64 banks.
-template <int NR>
-__device__ __forceinline__ int sub_off(int r, int c) {
-    return (c >> 5) * (NR * 64) + r * 64 + ((((c >> 3) & 3) ^ ((r >> 2) & 3)) << 4) + ((c & 7) << 1);
-}
-
-// One 1 KB direct load (16 bytes per lane) of rows 16 q .. 16 q + 15 of column block sb:
-// lane i fetches the global chunk that belongs at position i % 4 of row 16 q + i / 4.
-// Returns the chunk index (0..3) within the block; the caller supplies the global row.
-__device__ __forceinline__ int sub_chunk(int lane) { return (lane & 3) ^ ((lane >> 4) & 3); }
-
-// 8 consecutive columns c .. c + 7 (c % 8 == 0) of row r: one 16-byte read.
-template <int NR>
-__device__ __forceinline__ bf16x8 row8(const u32x4* tile, int r, int c) {
-    return *(const bf16x8*)((const char*)tile + sub_off<NR>(r, c));
-}
-
-// Operand fragment taken along a tile's rows: lane (n = lane % 32, hi = lane / 32) receives
-// tile[r0 + 8 hi + j][c0 + n], j = 0..7 (with PERM, column c0 + swap_b23(n)); r0 % 16 == 0
-// and c0 % 32 == 0.  Two ds_read_b64_tr_b16: in each group of 16 lanes, lane 4 a + e
-// receives element e of the 8 bytes addressed by lanes a, a + 4, a + 8, a + 12 of the group,
-// so lane i of a group addresses row r0 + 8 hi + i / 4 (+ 4 for the second read) at the
-// 4-column block that the result lanes with a = i % 4 need.
-template <int NR, bool PERM>
-__device__ __forceinline__ bf16x8 tr_frag(const u32x4* tile, int r0, int c0, int lane) {
-    const int G = lane >> 4, src = lane & 15, a = src & 3;
-    const int ap = PERM ? (((a & 1) << 1) | (a >> 1)) : a;
-    const int col = 16 * (G & 1) + 4 * ap;            // < 32
-    const int row = 8 * (G >> 1) + (src >> 2);         // < 16
-    const char* base = (const char*)tile + (c0 >> 5) * (NR * 64) + r0 * 64;
-    const v4i16 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + sub_off<NR>(row, col)));
-    const v4i16 up = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16*)(base + sub_off<NR>(row + 4, col)));
-    typedef short v8i16 __attribute__((ext_vector_type(8)));
-    const v8i16 v = __builtin_shufflevector(lo, up, 0, 1, 2, 3, 4, 5, 6, 7);
-    return __builtin_bit_cast(bf16x8, v);
-}
-
-// ---------------------------------------------------------------------------
-// Batched 2-D transpose: out[p][c][r] = in[p][r][c] for r < R, c < C, and 0 for
-// R <= r < Rp or C <= c < Cp.  64 x 64 tiles through LDS.
-// ---------------------------------------------------------------------------
+// out[c][r] = in[r][c]: 64 x 64 tiles through LDS (weights, once per layer).
 __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restrict__ in,
                                                         uint16_t* __restrict__ out, int R, int C,
-                                                        size_t in_ld, size_t in_plane, size_t out_ld,
-                                                        size_t out_plane, int Rp, int Cp, int tiles_r) {
+                                                        size_t in_ld, size_t out_ld) {
     __shared__ uint16_t t[64][66];
-    const int p = blockIdx.z;
-    const int r0 = (blockIdx.x % tiles_r) * 64, c0 = blockIdx.y * 64;
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
     const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-    const uint16_t* src = in + (size_t)p * in_plane;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
         const int r = r0 + ty + 4 * k, c = c0 + tx;
-        t[ty + 4 * k][tx] = (r < R && c < C) ? src[(size_t)r * in_ld + c] : (uint16_t)0;
+        t[ty + 4 * k][tx] = (r < R && c < C) ? in[(size_t)r * in_ld + c] : (uint16_t)0;
     }
     __syncthreads();
-    uint16_t* dst = out + (size_t)p * out_plane;
 #pragma unroll
     for (int k = 0; k < 16; ++k) {
         const int c = c0 + ty + 4 * k, r = r0 + tx;
-        if (c < Cp && r < Rp) dst[(size_t)c * out_ld + r] = t[tx][ty + 4 * k];
+        if (c < C && r < R) out[(size_t)c * out_ld + r] = t[tx][ty + 4 * k];
     }
 }
 
@@ -163,60 +112,34 @@ __global__ __launch_bounds__(256) void reduce_planes_kernel(const float* __restr
 }
 
 // ---------------------------------------------------------------------------
-// D = rowsum(dO * O) and O^T.  One workgroup per (64 tokens of the flattened B*S axis,
-// head); the O tile passes through LDS.  O^T is [a*128][Mp] with column = token, zero
-// for the tail [M, Mp).
+// D = rowsum(dO * O) for every (token, head): each group of 16 lanes takes one pair, 8
+// dims per lane (16 bytes of dO and of O), summed across the group.
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(256) void attn_bwd_prep_kernel(const uint16_t* __restrict__ dO,
                                                             const uint16_t* __restrict__ O,
-                                                            float* __restrict__ dsum,
-                                                            uint16_t* __restrict__ Ot, int B, int S,
-                                                            int Sp, int Mp, int a) {
-    __shared__ uint16_t tile[64][136];   // rows of 128 values + 8 of padding
-    const int nmt = Mp / 64;
-    const int mt = blockIdx.x % nmt, head = blockIdx.x / nmt;
-    const int m0 = mt * 64, M = B * S;
-    const int tid = threadIdx.x;
+                                                            float* __restrict__ dsum, int B, int S,
+                                                            int Sp, int a) {
+    const int M = B * S;
     const size_t ld = (size_t)a * D;
-    // Loads: thread t reads 4 x 16 bytes of row t / 4 (dims 32 (t % 4) .. + 31).
-    const int r = tid >> 2, q4 = tid & 3;
-    const int m = m0 + r;
+    const int item = blockIdx.x * 16 + (threadIdx.x >> 4);      // (token, head) pair
+    const int sub = threadIdx.x & 15;
+    const int m = item / a, head = item - (item / a) * a;
     float acc = 0.f;
     if (m < M) {
-        const size_t off = (size_t)m * ld + head * D + 32 * q4;
+        const size_t off = (size_t)m * ld + head * D + 8 * sub;
+        const u32x4 vd = *(const u32x4*)(dO + off);
+        const u32x4 vo = *(const u32x4*)(O + off);
 #pragma unroll
-        for (int k = 0; k < 4; ++k) {
-            const u32x4 vd = *(const u32x4*)(dO + off + 8 * k);
-            const u32x4 vo = *(const u32x4*)(O + off + 8 * k);
-            *(u32x4*)&tile[r][32 * q4 + 8 * k] = vo;
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                acc += __uint_as_float(vd[e] << 16) * __uint_as_float(vo[e] << 16);
-                acc += __uint_as_float(vd[e] & 0xFFFF0000u) * __uint_as_float(vo[e] & 0xFFFF0000u);
-            }
+        for (int e = 0; e < 4; ++e) {
+            acc += __uint_as_float(vd[e] << 16) * __uint_as_float(vo[e] << 16);
+            acc += __uint_as_float(vd[e] & 0xFFFF0000u) * __uint_as_float(vo[e] & 0xFFFF0000u);
         }
-    } else {
-#pragma unroll
-        for (int k = 0; k < 4; ++k) *(u32x4*)&tile[r][32 * q4 + 8 * k] = u32x4{0, 0, 0, 0};
     }
-    acc += __shfl_xor(acc, 1);
-    acc += __shfl_xor(acc, 2);
-    if (q4 == 0 && m < M) {
+#pragma unroll
+    for (int o = 8; o >= 1; o >>= 1) acc += __shfl_xor(acc, o);
+    if (sub == 0 && m < M) {
         const int b = m / S, s = m - b * S;
         dsum[((size_t)b * a + head) * Sp + s] = acc;
-    }
-    __syncthreads();
-    // Stores: O^T row d of the head, 8 tokens per 16-byte store; thread t writes rows
-    // t / 8 + 32 k, tokens 8 (t % 8) .. + 7.
-    const int c8 = tid & 7;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const int d = (tid >> 3) + 32 * k;
-        uint32_t w[4];
-#pragma unroll
-        for (int e = 0; e < 4; ++e)
-            w[e] = (uint32_t)tile[8 * c8 + 2 * e][d] | ((uint32_t)tile[8 * c8 + 2 * e + 1][d] << 16);
-        *(u32x4*)(Ot + (size_t)(head * D + d) * Mp + m0 + 8 * c8) = u32x4{w[0], w[1], w[2], w[3]};
     }
 }
 
@@ -248,9 +171,8 @@ struct KvArgs {
     float* acc_out_k;       // may alias acc_in_*
     float* acc_out_v;
     uint16_t* out;          // final rows [B*S][ldo] or null; dK at col_k + kvh*128, dV at col_v
-    uint16_t* outT;         // final transposed [*][Mp] (column = token) or null
     int ldo, col_k, col_v;
-    int B, S, Sp, Mp, a, g, cap;
+    int B, S, Sp, a, g, cap;
     float scale_log2, scale;
 };
 
@@ -420,16 +342,6 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
 #pragma unroll
             for (int nb = 0; nb < 4; ++nb) yk[nb] = yv[nb] = 0.f;
         }
-        // Transposed copy, column = token b * S + kk; the last sequence also writes the zero
-        // tail up to Mp.
-        const size_t col = (size_t)b * A.S + kk;
-        if (A.outT && (kk < A.S || (b == A.B - 1 && col < (size_t)A.Mp))) {
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb) {
-                A.outT[(size_t)(A.col_k + kvh * D + 32 * nb + l32) * A.Mp + col] = f2bf(yk[nb]);
-                A.outT[(size_t)(A.col_v + kvh * D + 32 * nb + l32) * A.Mp + col] = f2bf(yv[nb]);
-            }
-        }
     }
 }
 
@@ -450,10 +362,9 @@ struct QArgs {
     const uint16_t* kc;     // producer K slot [Bmax][g][cap][128]
     const uint16_t* vc;     // producer V slot [Bmax][g][128][cap]
     const float2* rope;     // [S][64]
-    uint16_t* out;          // dQ rows [B*S][ldo] at column head*128, or null
-    uint16_t* outT;         // dQ^T [a*128][Mp] (rows head*128 + d, column = token), or null
+    uint16_t* out;          // dQ rows [B*S][ldo] at column head*128
     int ldo;
-    int B, S, Sp, Mp, a, g, cap;
+    int B, S, Sp, a, g, cap;
     float scale_log2, scale;
 };
 
@@ -563,13 +474,8 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
     }
 
     // Epilogue: lane column = query ql; register e of block m holds dim
-    // 32 m + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate back (pairs m, m + 2), write rows
-    // and the transposed copy (column = token b * S + ql; the last sequence also writes
-    // the zero tail up to Mp).
-    const bool valid = ql < A.S;
-    const size_t col = (size_t)b * A.S + ql;
-    const bool tcol = valid || (b == A.B - 1 && col < (size_t)A.Mp);
-    if (valid || tcol) {
+    // 32 m + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate back (pairs m, m + 2), write.
+    if (ql < A.S) {
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
             float y[4][4];   // [block m][e % 4]
@@ -579,25 +485,18 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
                 for (int e4 = 0; e4 < 4; ++e4) {
                     const int e = 4 * g4 + e4;
                     const int i = 32 * m + 8 * g4 + 4 * hi + e4;
-                    const float2 cs = valid ? A.rope[(size_t)ql * 64 + i] : float2{1.f, 0.f};
+                    const float2 cs = A.rope[(size_t)ql * 64 + i];
                     const float x1 = dq[m][e] * A.scale, x2 = dq[m + 2][e] * A.scale;
-                    y[m][e4] = valid ? x1 * cs.x + x2 * cs.y : 0.f;
-                    y[m + 2][e4] = valid ? x2 * cs.x - x1 * cs.y : 0.f;
+                    y[m][e4] = x1 * cs.x + x2 * cs.y;
+                    y[m + 2][e4] = x2 * cs.x - x1 * cs.y;
                 }
 #pragma unroll
             for (int m = 0; m < 4; ++m) {
                 const int d0 = 32 * m + 8 * g4 + 4 * hi;
-                if (A.out && valid) {
-                    u32x2 w;
-                    w[0] = pack2bf(y[m][0], y[m][1]);
-                    w[1] = pack2bf(y[m][2], y[m][3]);
-                    *(u32x2*)(A.out + ((size_t)b * A.S + ql) * A.ldo + head * D + d0) = w;
-                }
-                if (A.outT && tcol) {
-#pragma unroll
-                    for (int e4 = 0; e4 < 4; ++e4)
-                        A.outT[(size_t)(head * D + d0 + e4) * A.Mp + col] = f2bf(y[m][e4]);
-                }
+                u32x2 w;
+                w[0] = pack2bf(y[m][0], y[m][1]);
+                w[1] = pack2bf(y[m][2], y[m][3]);
+                *(u32x2*)(A.out + ((size_t)b * A.S + ql) * A.ldo + head * D + d0) = w;
             }
         }
     }
@@ -605,13 +504,11 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
 
 }  // namespace
 
-hipError_t transpose_bf16(const uint16_t* in, uint16_t* out, int planes, int R, int C, size_t in_ld,
-                          size_t in_plane, size_t out_ld, size_t out_plane, int Rp, int Cp,
+hipError_t transpose_bf16(const uint16_t* in, uint16_t* out, int R, int C, size_t in_ld, size_t out_ld,
                           hipStream_t st) {
-    const int tr = (Rp + 63) / 64, tc = (Cp + 63) / 64;
-    if (planes < 1 || tr < 1 || tc < 1) return hipSuccess;
-    hipLaunchKernelGGL(transpose_kernel, dim3(tr, tc, planes), dim3(256), 0, st, in, out, R, C, in_ld,
-                       in_plane, out_ld, out_plane, Rp, Cp, tr);
+    if (R < 1 || C < 1) return hipSuccess;
+    hipLaunchKernelGGL(transpose_kernel, dim3((R + 63) / 64, (C + 63) / 64), dim3(256), 0, st, in, out, R, C,
+                       in_ld, out_ld);
     return hipGetLastError();
 }
 
@@ -632,10 +529,10 @@ hipError_t reduce_planes(const float* part, int planes, int M, int N, float* dst
     return hipGetLastError();
 }
 
-hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, float* dsum, uint16_t* Ot, int B,
-                              int S, int Sp, int Mp, int a, hipStream_t st) {
-    hipLaunchKernelGGL(attn_bwd_prep_kernel, dim3((Mp / 64) * a), dim3(256), 0, st, dO, O, dsum, Ot, B, S,
-                       Sp, Mp, a);
+hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, float* dsum, int B, int S, int Sp, int a,
+                              hipStream_t st) {
+    const int items = B * S * a;
+    hipLaunchKernelGGL(attn_bwd_prep_kernel, dim3((items + 15) / 16), dim3(256), 0, st, dO, O, dsum, B, S, Sp, a);
     return hipGetLastError();
 }
 
@@ -643,8 +540,8 @@ hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
     KvArgs A;
     A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.vc = p.vc; A.rope = p.rope;
     A.acc_in_k = p.acc_in_k; A.acc_in_v = p.acc_in_v; A.acc_out_k = p.acc_out_k; A.acc_out_v = p.acc_out_v;
-    A.out = p.out; A.outT = p.outT; A.ldo = p.ldo; A.col_k = p.col_k; A.col_v = p.col_v;
-    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.Mp = p.Mp; A.a = p.a; A.g = p.g; A.cap = p.cap;
+    A.out = p.out; A.ldo = p.ldo; A.col_k = p.col_k; A.col_v = p.col_v;
+    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int nkb = (p.S + KV_BK - 1) / KV_BK;
@@ -655,8 +552,8 @@ hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
 hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st) {
     QArgs A;
     A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.vc = p.vc;
-    A.rope = p.rope; A.out = p.out; A.outT = p.outT; A.ldo = p.ldo;
-    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.Mp = p.Mp; A.a = p.a; A.g = p.g; A.cap = p.cap;
+    A.rope = p.rope; A.out = p.out; A.ldo = p.ldo;
+    A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
     const int nqt = (p.S + Q_BQ - 1) / Q_BQ;

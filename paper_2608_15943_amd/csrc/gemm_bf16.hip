@@ -20,6 +20,7 @@
 // M-panels (its own L2 keeps the A and W panels hot).
 #include "common.h"
 #include "kernels.h"
+#include "lds_tr.h"
 
 namespace kvp {
 namespace {
@@ -476,6 +477,149 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
     }
 }
 
+// ---------------------------------------------------------------------------
+// The same tiling for C[M][N] = sum_k A[k][m] B[k][n] with both operands given K-major
+// ([K][rows], rows contiguous): the weight gradients dW_O = G^T O and
+// dW_QKV = [dQ|dK|dV]^T X of the backward, whose K is the token axis.  Each operand tile is
+// staged as [64 k][256 rows] in the sub-tiled layout and its MFMA fragments are taken along
+// the tile's rows with the LDS transpose read (two ds_read_b64_tr_b16 each), so neither
+// operand is copied transposed.  Any K: the last tile reads clamped rows, and the A
+// fragments zero the rows past K.  (For products with K-major weights, dO = G W_O and
+// dX += [dQ|dK|dV] W_stack, the row-major kernel on once-transposed weights is faster: the
+// transpose read moves 8 bytes per lane per instruction against 16.)
+// ---------------------------------------------------------------------------
+// A K-major operand: k-rows of `ld` values, stacked from up to three buffers (p[i] holds
+// rows[i] k-rows).  Written this way (templated operand, if-constexpr'd loads) the kernel
+// compiles to 384 registers without spills; a plain single-pointer spelling of the same
+// loop was compiled to 512 registers plus 130-180 spilled ones, 2.6x slower.
+template <bool T>
+struct Operand {
+    WRows w;
+    int ld;
+    __device__ __forceinline__ const uint16_t* krow(int k) const {
+        if (k < w.rows[0]) return (const uint16_t*)w.p[0] + (size_t)k * ld;
+        k -= w.rows[0];
+        if (k < w.rows[1]) return (const uint16_t*)w.p[1] + (size_t)k * ld;
+        k -= w.rows[1];
+        return (const uint16_t*)w.p[2] + (size_t)k * ld;
+    }
+};
+
+template <class Epi, bool TA, bool TB>
+__global__ __launch_bounds__(NT, 1) void gemm_bf16_g(Operand<TA> Aop, Operand<TB> Bop, int M, int N, int K,
+                                                    int splits, Epi epi) {
+    __shared__ u32x4 lds[2][2][BM * 8];  // [stage][A, B]: [64 k][256] bf16, sub-tiled
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int wm = wave >> 1, wn = wave & 1;
+    const int l32 = lane & 31, hi = lane >> 5;
+    const int ntm = (M + BM - 1) / BM, ntn = (N + BN - 1) / BN;
+    const int lid0 = xcd_remap(blockIdx.x, gridDim.x);
+    const int split = lid0 / (ntm * ntn);
+    const int lid = lid0 - split * (ntm * ntn);
+    epi.set_split(split);
+    const int group = lid / (GROUP_M * ntn), first = group * GROUP_M;
+    const int gsz = min(ntm - first, GROUP_M);
+    const int in_g = lid - group * GROUP_M * ntn;
+    const int m0 = (first + in_g % gsz) * BM, n0 = (in_g / gsz) * BN;
+    const int nkt = (K + BK - 1) / BK;
+    const int kt0 = split * nkt / splits, kt1 = (split + 1) * nkt / splits;
+    const int ch = sub_chunk(lane);
+    auto tsrc = [&](const auto& op, int c0, int C, int kt, int j) {
+        const int u = 8 * wave + j, sb = u >> 2, q = u & 3;
+        const int k = min(kt * BK + 16 * q + (lane >> 2), K - 1);
+        const int col = min(c0 + 32 * sb + 8 * ch, C - 8);
+        return op.krow(k) + col;
+    };
+    auto issue_part = [&](int kt, int stg, int j) {
+        if constexpr (TA) {
+            const int u = 8 * wave + j;
+            __builtin_amdgcn_global_load_lds((gvoid_t*)tsrc(Aop, m0, M, kt, j),
+                                             (lvoid_t*)((char*)&lds[stg][0][0] + (u >> 2) * 4096 + (u & 3) * 1024),
+                                             16, 0, 0);
+        }
+        if constexpr (TB) {
+            const int u = 8 * wave + j;
+            __builtin_amdgcn_global_load_lds((gvoid_t*)tsrc(Bop, n0, N, kt, j),
+                                             (lvoid_t*)((char*)&lds[stg][1][0] + (u >> 2) * 4096 + (u & 3) * 1024),
+                                             16, 0, 0);
+        }
+    };
+    auto issue = [&](int kt, int stg) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) issue_part(kt, stg, j);
+    };
+    f32x16 acc[4][4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    const bool ktail = TA && (K % BK) != 0;
+    auto load_frags = [&](int stg, int kt, int ks, bf16x8 (&fa)[4], bf16x8 (&fb)[4]) {
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+            if constexpr (TA) fa[i] = tr_frag<BK, false>(lds[stg][0], 16 * ks, wm * 128 + 32 * i, lane);
+            if constexpr (TB) fb[i] = tr_frag<BK, false>(lds[stg][1], 16 * ks, wn * 128 + 32 * i, lane);
+        }
+        if (ktail && kt == nkt - 1) {
+            const int kb = kt * BK + 16 * ks + 8 * hi;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                u32x4 v = __builtin_bit_cast(u32x4, fa[i]);
+#pragma unroll
+                for (int e = 0; e < 4; ++e)
+                    v[e] &= (kb + 2 * e < K ? 0x0000FFFFu : 0u) | (kb + 2 * e + 1 < K ? 0xFFFF0000u : 0u);
+                fa[i] = __builtin_bit_cast(bf16x8, v);
+            }
+        }
+    };
+    (void)l32;
+    if (kt0 < kt1) {
+        issue(kt0, 0);
+        asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+        __syncthreads();
+        bf16x8 fa[4], fb[4], ga[4], gb[4];
+        load_frags(0, kt0, 0, fa, fb);
+        for (int kt = kt0; kt < kt1; ++kt) {
+            const int cur = (kt - kt0) & 1;
+            const bool more = kt + 1 < kt1;
+#pragma unroll
+            for (int ks = 0; ks < 4; ++ks) {
+                if (more && ks < 2) {
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) issue_part(kt + 1, cur ^ 1, 4 * ks + j);
+                }
+                if (ks < 3) load_frags(cur, kt, ks + 1, ga, gb);
+#pragma unroll
+                for (int mb = 0; mb < 4; ++mb)
+#pragma unroll
+                    for (int nb2 = 0; nb2 < 4; ++nb2) acc[mb][nb2] = mfma32x32x16(fa[mb], fb[nb2], acc[mb][nb2]);
+                if (ks < 3) {
+#pragma unroll
+                    for (int i = 0; i < 4; ++i) {
+                        fa[i] = ga[i];
+                        fb[i] = gb[i];
+                    }
+                }
+            }
+            if (more) {
+                asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+                __syncthreads();
+                load_frags(cur ^ 1, kt + 1, 0, fa, fb);
+            }
+        }
+    }
+    char* st = (char*)&lds[0][0][0] + wave * 32768;
+#pragma unroll
+    for (int pass = 0; pass < Epi::kPasses; ++pass) {
+        __syncthreads();
+        typename Epi::Pre pre;
+        epi.prefetch(pass, m0 + wm * 128, n0 + wn * 128, lane, M, N, pre);
+        epi.stage(pass, acc, m0 + wm * 128, n0 + wn * 128, lane, M, N, st);
+        __syncthreads();
+        epi.flush(pass, m0 + wm * 128, n0 + wn * 128, lane, M, N, st, pre);
+    }
+}
+
 template <class Epi>
 hipError_t launch(const uint16_t* A, const WRows& W, int M, int N, int K, const Epi& epi,
                   hipStream_t st, int splits = 1) {
@@ -499,20 +643,33 @@ hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_r
     return launch(a, W, M, N, K, ResidEpi<false>{x_res, y, yf}, st);
 }
 
-int gemm_out_splits(int M, int N, int K) {
+hipError_t gemm_kmajor_out_bf16(const uint16_t* a, int lda, const uint16_t* b, int ldb, int M, int N, int K,
+                                int splits, float* part, hipStream_t st) {
+    if (splits < 1 || splits > (K + BK - 1) / BK || M % 8 || N % 8 || lda % 8 || ldb % 8)
+        return hipErrorInvalidValue;
+    Operand<true> A{{{a, nullptr, nullptr}, {K, 0, 0}}, lda};
+    Operand<true> B{{{b, nullptr, nullptr}, {K, 0, 0}}, ldb};
     const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    const int nk = K / BK;
-    int s = 1;
-    // One workgroup per CU: split K until the grid covers the 256 CUs (at most 8 slices).
-    while (tiles * s < 256 && s < 8 && nk % (2 * s) == 0) s *= 2;
-    return s;
+    hipLaunchKernelGGL((gemm_bf16_g<OutEpi, true, true>), dim3(tiles * splits), dim3(NT), 0, st, A, B, M, N, K,
+                       splits, OutEpi{part, (size_t)M * N, 0, false});
+    return hipGetLastError();
 }
 
-hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits,
-                         void* part, bool bf16_out, hipStream_t st) {
+hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, uint16_t* c,
+                         hipStream_t st) {
+    if (K % BK) return hipErrorInvalidValue;
     WRows W{{w, nullptr, nullptr}, {N, 0, 0}};
-    if (splits < 1 || (K / BK) % splits || (bf16_out && splits != 1)) return hipErrorInvalidValue;
-    return launch(a, W, M, N, K, OutEpi{part, (size_t)M * N, 0, bf16_out}, st, splits);
+    return launch(a, W, M, N, K, OutEpi{c, 0, 0, true}, st);
+}
+
+int gemm_out_splits(int M, int N, int K) {
+    const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
+    const int nkt = (K + BK - 1) / BK;
+    int s = 1;
+    // One workgroup per CU: split K until the grid covers the 256 CUs (at most 8 slices, each
+    // at least one 64-wide tile).
+    while (tiles * s < 256 && 2 * s <= 8 && 2 * s <= nkt) s *= 2;
+    return s;
 }
 
 }  // namespace kvp

@@ -40,30 +40,31 @@ hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint1
                               uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
                               hipStream_t st);
 
-// C = A @ W^T (A [M][K], W [N][K], K % 64 == 0) split over `splits` equal slices of K:
-// slice s writes its fp32 partial sum to part + s * M * N ([M][N] each), or, with
-// bf16_out, a single slice writes bf16 C [M][N] to part.
-hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits,
-                         void* part, bool bf16_out, hipStream_t st);
-// The slice count gemm_out_bf16 should use for an M x N x K product on this device.
+// The slice count gemm_kmajor_out_bf16 should use for an M x N x K product.
 int gemm_out_splits(int M, int N, int K);
+
+// C[M][N] = sum_k a[k][m] b[k][n] with a [K][lda], b [K][ldb] K-major (the backward's weight
+// gradients; any K; M, N, lda, ldb % 8 == 0), split over `splits` ranges of whole 64-wide K
+// tiles, fp32 partials to part + s * M * N.
+hipError_t gemm_kmajor_out_bf16(const uint16_t* a, int lda, const uint16_t* b, int ldb, int M, int N, int K,
+                                int splits, float* part, hipStream_t st);
+// C = a @ w^T in bf16 (a [M][K], w [N][K], K % 64 == 0), no fused work.
+hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, uint16_t* c,
+                         hipStream_t st);
 
 // ---- bf16 backward ----------------------------------------------------------
 
-// out[p][c][r] = in[p][r][c] (r < R, c < C), zero for R <= r < Rp, C <= c < Cp.
-hipError_t transpose_bf16(const uint16_t* in, uint16_t* out, int planes, int R, int C, size_t in_ld,
-                          size_t in_plane, size_t out_ld, size_t out_plane, int Rp, int Cp,
+// out[c][r] = in[r][c] for r < R, c < C (row strides in_ld, out_ld).
+hipError_t transpose_bf16(const uint16_t* in, uint16_t* out, int R, int C, size_t in_ld, size_t out_ld,
                           hipStream_t st);
 hipError_t f32_to_bf16(const float* x, uint16_t* y, size_t n, hipStream_t st);
 // Sum of `planes` [M][N] fp32 planes; rows [0, rows0) -> dst0, then rows1 -> dst1, rest -> dst2.
 hipError_t reduce_planes(const float* part, int planes, int M, int N, float* dst0, int rows0, float* dst1,
                          int rows1, float* dst2, hipStream_t st);
-// D = rowsum(dO * O) [B][a][Sp] and O^T [a*128][Mp] (column = token, zero tail).
-hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, float* dsum, uint16_t* Ot, int B,
-                              int S, int Sp, int Mp, int a, hipStream_t st);
+// D = rowsum(dO * O) [B][a][Sp].
+hipError_t attn_bwd_prep_bf16(const uint16_t* dO, const uint16_t* O, float* dsum, int B, int S, int Sp, int a,
+                              hipStream_t st);
 
-// Transposed outputs (outT) are [rows][Mp] with column = token b * S + s, Mp = B * S
-// rounded up to 64, zero tail.
 struct AttnBwdKv {
     const uint16_t* q;      // post-RoPE Q of the layer [B*S][a*128]
     const uint16_t* dO;     // [B*S][a*128]
@@ -77,9 +78,8 @@ struct AttnBwdKv {
     float* acc_out_k;
     float* acc_out_v;
     uint16_t* out;
-    uint16_t* outT;
     int ldo, col_k, col_v;
-    int B, S, Sp, Mp, a, g, cap;
+    int B, S, Sp, a, g, cap;
 };
 hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st);
 
@@ -92,9 +92,8 @@ struct AttnBwdQ {
     const uint16_t* vc;
     const float2* rope;
     uint16_t* out;
-    uint16_t* outT;
     int ldo;
-    int B, S, Sp, Mp, a, g, cap;
+    int B, S, Sp, a, g, cap;
 };
 hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st);
 

@@ -540,11 +540,9 @@ Saved saved_layout(const kvp_ctx& c, int B, int S) {
     return v;
 }
 
-// Workspace of kvp_backward.  Transposed activations are [rows][Mp], column = token
-// (Mp = B * S rounded up to 64, zero tail).
+// Workspace of kvp_backward.
 struct BwdWs {
-    size_t gb = 0, gbt = 0, dO = 0, ot = 0, xt = 0, dsum = 0, dqkv = 0, dqkvt = 0;
-    size_t acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
+    size_t gb = 0, dO = 0, dsum = 0, dqkv = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
     size_t acc_plane = 0;          // floats of one dK or dV sum
     std::vector<int> acc_slot;     // per layer: index of its fp32 sum pair, or -1
 };
@@ -557,16 +555,12 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
         off += align_up(bytes);
         return at;
     };
-    const size_t M = (size_t)B * S, Mp = round64((int)M);
+    const size_t M = (size_t)B * S;
     const size_t h = c.d.h, nq = c.n_q(), nkv = c.n_kv(), np = nq + 2 * nkv;
     w.gb = take(M * h * 2);
-    w.gbt = take(h * Mp * 2);
     w.dO = take(M * nq * 2);
-    w.ot = take(nq * Mp * 2);
-    w.xt = take(h * Mp * 2);
     w.dsum = take((size_t)B * c.d.a * round64(S) * sizeof(float));
     w.dqkv = take(M * np * 2);
-    w.dqkvt = take(np * Mp * 2);
     // One fp32 dK/dV pair per producer that has consumers.
     w.acc_slot.assign(c.d.L, -1);
     int nacc = 0;
@@ -579,12 +573,12 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
                 }
     w.acc_plane = (size_t)B * c.d.g * S * 128;
     w.acc = take((size_t)nacc * 2 * w.acc_plane * sizeof(float));
-    w.wot = take(nq * h * 2);
-    w.wst = take(h * np * 2);
+    w.wot = take(nq * h * 2);   // W_O^T [a*d_h][h]
+    w.wst = take(h * np * 2);   // [W_Q; W_K; W_V]^T [h][np]
     // Split-K partial planes of the weight-gradient GEMMs (consumers: Q rows only).
-    const int so = kvp::gemm_out_splits((int)h, (int)nq, (int)Mp);
-    const int sp = kvp::gemm_out_splits((int)np, (int)h, (int)Mp);
-    const int sc = kvp::gemm_out_splits((int)nq, (int)h, (int)Mp);
+    const int so = kvp::gemm_out_splits((int)h, (int)nq, (int)M);
+    const int sp = kvp::gemm_out_splits((int)np, (int)h, (int)M);
+    const int sc = kvp::gemm_out_splits((int)nq, (int)h, (int)M);
     w.part = take(std::max({(size_t)so * h * nq, (size_t)sp * np * h, (size_t)sc * nq * h}) * sizeof(float));
     w.rope = take((size_t)S * 64 * sizeof(float2));
     w.total = off;
@@ -787,8 +781,8 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
     if (B > ctx->d.max_batch || S > ctx->d.max_seq)
         return fail(KVP_E_CAPACITY, "kvp_backward: B=%d, S=%d exceed max_batch / max_seq", B, S);
     const int h = ctx->d.h, nq = ctx->n_q(), nkv = ctx->n_kv(), L = ctx->d.L;
-    const int Sp = round64(S), M = B * S, Mp = round64(M);
-    if ((int64_t)(nq + 2 * nkv) * Mp > INT32_MAX || (int64_t)M * std::max(h, nq + 2 * nkv) > INT32_MAX)
+    const int Sp = round64(S), M = B * S;
+    if ((int64_t)M * std::max(h, nq + 2 * nkv) > INT32_MAX)
         return fail(KVP_E_SHAPE, "kvp_backward: sizes exceed the 32-bit index range");
     const Saved sv = saved_layout(*ctx, B, S);
     if (!saved || saved_bytes < sv.total || !aligned16(saved))
@@ -808,8 +802,7 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
     char* base = (char*)ws;
     const char* sb = (const char*)saved;
     auto bp = [&](size_t off) { return (uint16_t*)(base + off); };
-    uint16_t *gb = bp(w.gb), *gbt = bp(w.gbt), *dO = bp(w.dO), *ot = bp(w.ot), *xt = bp(w.xt),
-             *dqkv = bp(w.dqkv), *dqkvt = bp(w.dqkvt), *wot = bp(w.wot), *wst = bp(w.wst);
+    uint16_t *gb = bp(w.gb), *dO = bp(w.dO), *dqkv = bp(w.dqkv), *wot = bp(w.wot), *wst = bp(w.wst);
     float* dsum = (float*)(base + w.dsum);
     float* acc = (float*)(base + w.acc);
     float* part = (float*)(base + w.part);
@@ -837,27 +830,20 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         const float* lse = (const float*)(lay + sv.lse);
         const uint16_t* Xl = l == 0 ? (const uint16_t*)x : (const uint16_t*)(lay + sv.x);
 
-        // dO = G W_O (W_O^T as the [a*d_h][h] operand), then D and the transposed copies.
+        // dO = G W_O (on W_O^T), D = rowsum(dO * O), dW_O = G^T O (both K-major over the tokens).
         if ((rc = aux([&] {
-                 return check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wo, wot, 1, h, nq, nq, 0, h, 0, h, nq, st),
-                                  "transpose W_O");
+                 return check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wo, wot, h, nq, nq, h, st), "transpose W_O");
              })))
             return rc;
-        if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gb, wot, M, nq, h, 1, dO, true, st), "dO GEMM"); })))
+        if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gb, wot, M, nq, h, dO, st), "dO GEMM"); })))
             return rc;
         if ((rc = aux([&] {
-                 return check_hip(kvp::attn_bwd_prep_bf16(dO, Ol, dsum, ot, B, S, Sp, Mp, ctx->d.a, st),
-                                  "attention backward prep");
-             })))
-            return rc;
-        // dW_O = G^T O.
-        if ((rc = aux([&] {
-                 return check_hip(kvp::transpose_bf16(gb, gbt, 1, M, h, h, 0, Mp, 0, Mp, h, st), "transpose G");
+                 return check_hip(kvp::attn_bwd_prep_bf16(dO, Ol, dsum, B, S, Sp, ctx->d.a, st), "attention backward D");
              })))
             return rc;
         {
-            const int s = kvp::gemm_out_splits(h, nq, Mp);
-            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(gbt, ot, h, nq, Mp, s, part, false, st), "dW_O GEMM"); })))
+            const int s = kvp::gemm_out_splits(h, nq, M);
+            if ((rc = gemm([&] { return check_hip(kvp::gemm_kmajor_out_bf16(gb, h, Ol, nq, h, nq, M, s, part, st), "dW_O GEMM"); })))
                 return rc;
             if ((rc = aux([&] {
                      return check_hip(kvp::reduce_planes(part, s, h, nq, Ly.dwo, h, nullptr, 0, nullptr, st), "dW_O sum");
@@ -882,12 +868,11 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
                 a.acc_in_k = acc_written[l] ? ak : nullptr;
                 a.acc_in_v = acc_written[l] ? av : nullptr;
                 a.out = dqkv;
-                a.outT = dqkvt;
                 a.ldo = np;
                 a.col_k = nq;
                 a.col_v = nq + nkv;
             }
-            a.B = B; a.S = S; a.Sp = Sp; a.Mp = Mp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
+            a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
             if ((rc = timed(ctx, KVP_K_BWD_ATTN_KV, st, [&] {
                      return check_hip(kvp::flash_bwd_kv_bf16(a, st), "attention backward dK dV");
                  })))
@@ -896,21 +881,19 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         {
             kvp::AttnBwdQ a{};
             a.q = Ql; a.dO = dO; a.lse = lse; a.dsum = dsum; a.kc = (const uint16_t*)Pl.kc;
-            a.vc = (const uint16_t*)Pl.vc; a.rope = rope; a.out = dqkv; a.outT = dqkvt; a.ldo = np;
-            a.B = B; a.S = S; a.Sp = Sp; a.Mp = Mp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
+            a.vc = (const uint16_t*)Pl.vc; a.rope = rope; a.out = dqkv; a.ldo = np;
+            a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
             if ((rc = timed(ctx, KVP_K_BWD_ATTN_Q, st, [&] {
                      return check_hip(kvp::flash_bwd_q_bf16(a, st), "attention backward dQ");
                  })))
                 return rc;
         }
-        // dW_Q (| dW_K | dW_V) = [dQ | dK | dV]^T X_l.
-        if ((rc = aux([&] {
-                 return check_hip(kvp::transpose_bf16(Xl, xt, 1, M, h, h, 0, Mp, 0, Mp, h, st), "transpose X");
-             })))
-            return rc;
+        // dW_Q (| dW_K | dW_V) = [dQ | dK | dV]^T X_l (both K-major over the tokens).
         {
-            const int s = kvp::gemm_out_splits(np, h, Mp);
-            if ((rc = gemm([&] { return check_hip(kvp::gemm_out_bf16(dqkvt, xt, np, h, Mp, s, part, false, st), "dW_QKV GEMM"); })))
+            const int s = kvp::gemm_out_splits(np, h, M);
+            if ((rc = gemm([&] {
+                     return check_hip(kvp::gemm_kmajor_out_bf16(dqkv, np, Xl, h, np, h, M, s, part, st), "dW_QKV GEMM");
+                 })))
                 return rc;
             if ((rc = aux([&] {
                      return check_hip(kvp::reduce_planes(part, s, np, h, Ly.dwq, nq, Ly.dwk, producer ? nkv : 0,
@@ -919,26 +902,26 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
                  })))
                 return rc;
         }
-        // G += [dQ | dK | dV] [W_Q; W_K; W_V] (the stacked weights transposed to [h][np]).
+        // dX_l = dX_{l+1} + [dQ | dK | dV] [W_Q; W_K; W_V] (on the stacked weights transposed
+        // to [h][np]).
         if ((rc = aux([&] {
-                 int r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wq, wst, 1, nq, h, h, 0, np, 0, nq, h, st),
-                                    "transpose W_Q");
+                 int r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wq, wst, nq, h, h, np, st), "transpose W_Q");
                  if (!r2 && producer)
-                     r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wk, wst + nq, 1, nkv, h, h, 0, np, 0, nkv,
-                                                        h, st),
+                     r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wk, wst + nq, nkv, h, h, np, st),
                                     "transpose W_K");
                  if (!r2 && producer)
-                     r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wv, wst + nq + nkv, 1, nkv, h, h, 0, np, 0,
-                                                        nkv, h, st),
+                     r2 = check_hip(kvp::transpose_bf16((const uint16_t*)Ly.wv, wst + nq + nkv, nkv, h, h, np, st),
                                     "transpose W_V");
                  return r2;
              })))
             return rc;
-        const void* gres = l == L - 1 ? dy : dx;
-        if ((rc = gemm([&] {
-                 return check_hip(kvp::gemm_resid_bf16(dqkv, wst, gres, true, gb, (float*)dx, M, h, np, st), "dX GEMM");
-             })))
-            return rc;
+        {
+            const void* gres = l == L - 1 ? dy : dx;
+            if ((rc = gemm([&] {
+                     return check_hip(kvp::gemm_resid_bf16(dqkv, wst, gres, true, gb, (float*)dx, M, h, np, st), "dX GEMM");
+                 })))
+                return rc;
+        }
     }
     return ok();
 }
