@@ -279,10 +279,10 @@ int kvp_set_kv_slot(kvp_ctx* ctx, int l, void* K, void* V);
  * batch B and length S (prefill, backward; ignored for decode) needs.  The
  * workspace holds Q, the attention output, the fp32 residual stream and its
  * bf16 copy, the RoPE table (prefill) and split-K partial results (decode);
- * for KVP_PHASE_BACKWARD (bf16 models) the gradients in flight, their
- * transposed copies, transposed weights and the producers' fp32 dK/dV sums.
- * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY (B > max_batch, S > max_seq),
- * KVP_E_SHAPE (backward of an fp32 model).
+ * for KVP_PHASE_BACKWARD the gradients in flight, (bf16 models) their
+ * transposed copies and transposed weights, (fp32 models) the per-(token,
+ * head) softmax statistics, and the producers' fp32 dK/dV sums.
+ * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY (B > max_batch, S > max_seq).
  */
 int kvp_workspace_size(const kvp_ctx* ctx, int phase, int B, int S, size_t* bytes);
 
@@ -327,12 +327,13 @@ int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max
 /* ======================================================================== */
 /*
  * Training a KV-shared model (the setting of Sec. 3) needs the gradients of the
- * stack above.  bf16 models only (KVP_E_SHAPE for fp32).  The forward keeps, per
- * layer l, in the caller's `saved` buffer: the post-RoPE Q_l and the attention
- * output O_l ([B*S, a*d_h] bf16), the bf16 layer input X_l for l >= 1
- * ([B*S, h]; X_0 is the caller's x), and the row log-sum-exp of the scaled
- * scores ([B, a, Sp] fp32, log2 domain, Sp = S rounded up to 64).  The producers'
- * K/V slots hold what the forward wrote; the backward reads them.
+ * stack above.  The forward keeps, per layer l, in the caller's `saved` buffer,
+ * in the model dtype: the post-RoPE Q_l and the attention output O_l
+ * ([B*S, a*d_h]), the layer input X_l for l >= 1 ([B*S, h]; X_0 is the
+ * caller's x), and for bf16 models the row log-sum-exp of the scaled scores
+ * ([B, a, Sp] fp32, log2 domain, Sp = S rounded up to 64; fp32 models
+ * recompute it).  The producers' K/V slots hold what the forward wrote; the
+ * backward reads them.
  *
  * The backward runs the layers last to first.  For layer l with producer
  * p = tau(l): dW_O = G^T O_l and dO = G W_O with G = dLoss/dX_{l+1}; the
@@ -340,19 +341,19 @@ int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max
  * through RoPE); a consumer adds its dK, dV to an fp32 buffer of its producer,
  * and the producer adds that sum to its own (Eq. 3: K_p, V_p feed every layer
  * that maps to p); then dW_Q = dQ^T X_l, for a producer dW_K = dK^T X_l and
- * dW_V = dV^T X_l, and G += dQ W_Q (+ dK W_K + dV W_V).  Products on bf16
- * matrix cores with fp32 accumulation; G is carried in fp32.
+ * dW_V = dV^T X_l, and G += dQ W_Q (+ dK W_K + dV W_V).  bf16 models: products
+ * on bf16 matrix cores with fp32 accumulation, G carried in fp32.  fp32 models:
+ * every step in fp32 on the vector ALUs.
  */
 
 /* kvp_train_saved_size -- bytes of the `saved` buffer for a call with B, S.
- * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY, KVP_E_SHAPE (fp32 model). */
+ * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY. */
 int kvp_train_saved_size(const kvp_ctx* ctx, int B, int S, size_t* bytes);
 
 /*
  * kvp_train_forward -- kvp_prefill that also fills `saved` (16-byte aligned,
  * at least kvp_train_saved_size bytes).  Workspace: KVP_PHASE_PREFILL.
- * Errors: as kvp_prefill, plus KVP_E_WORKSPACE for a short `saved` buffer and
- * KVP_E_SHAPE for an fp32 model.
+ * Errors: as kvp_prefill, plus KVP_E_WORKSPACE for a short `saved` buffer.
  */
 int kvp_train_forward(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* saved,
                       size_t saved_bytes, void* ws, size_t ws_bytes, void* stream);
@@ -370,7 +371,9 @@ int kvp_set_layer_grads(kvp_ctx* ctx, int l, void* dWq, void* dWk, void* dWv, vo
  * kvp_backward -- gradients of the last kvp_train_forward with the same x,
  * B, S and saved buffer: dy = dLoss/dY [B*S, h] fp32 in, dx = dLoss/dX_0
  * [B*S, h] fp32 out (dx must not alias dy or x), weight gradients into the
- * buffers of kvp_set_layer_grads.  Workspace: KVP_PHASE_BACKWARD.
+ * buffers of kvp_set_layer_grads.  Workspace: KVP_PHASE_BACKWARD.  For fp32
+ * models x is the fp32 input and the whole attention backward of a layer is
+ * timed as KVP_K_BWD_ATTN_KV.
  * Errors: KVP_E_INVALID_ARG, KVP_E_CAPACITY, KVP_E_WORKSPACE, KVP_E_SHAPE,
  * KVP_E_STATE (weights, slots or gradient buffers of some layer not set),
  * KVP_E_HIP.

@@ -154,4 +154,37 @@ hipError_t gemm_f32(const float* a, const WRows& w, int M, int N, int K, float* 
 hipError_t attn_f32(const float* q, const float* kc, const float* vc, const int32_t* lens,
                     float* o, int rows, int S, int a, int g, int d, int cap, hipStream_t st);
 
+// ---- fp32 backward (vector ALU) ---------------------------------------------
+
+// C[m][n] = R[m][n] + sum_k A(m, k) B(k, n) with A(m, k) = a[m * sam + k * sak] and
+// B(k, n) = b[k * sbk + n * sbn]; R = res (row stride ldc, may equal c) or 0 when null.
+hipError_t gemm_f32_strided(const float* a, size_t sam, size_t sak, const float* b, size_t sbk, size_t sbn,
+                            const float* res, float* c, size_t ldc, int M, int N, int K, hipStream_t st);
+
+// Attention backward of one fp32 layer: q, dO, O [B*S][a*d] (q after RoPE), the producer's
+// K slot [B][g][cap][d] and V slot [B][g][d][cap]; lse and dsum [B*S*a] are scratch.
+// dQ (rotated back, scaled) goes to out_q columns h*d of rows ldo floats apart.  dK, dV
+// (dK rotated back and scaled) plus acc_in_* (optional, [B][g][S][d]) go to acc_out_* (same
+// layout, may equal acc_in_*) and / or to out_kv row b*S + key at columns col_k / col_v +
+// kvh*d.  d in {16, 32, 64, 128}.
+struct AttnBwdF32 {
+    const float* q;
+    const float* dO;
+    const float* O;
+    const float* kc;
+    const float* vc;
+    const float2* rope;     // [S][d/2] (cos, sin)
+    float* lse;
+    float* dsum;
+    const float* acc_in_k;
+    const float* acc_in_v;
+    float* acc_out_k;
+    float* acc_out_v;
+    float* out_kv;
+    float* out_q;
+    int ldo, col_k, col_v;
+    int B, S, a, g, d, cap;
+};
+hipError_t attn_bwd_f32(const AttnBwdF32& p, hipStream_t st);
+
 }  // namespace kvp

@@ -258,7 +258,7 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
         });
     }
     float* proj = (float*)(ws + w.proj);
-    float* q = (float*)(ws + w.q);
+    float* q = (float*)(q_buf ? q_buf : ws + w.q);
     if ((rc = timed(c, KVP_K_QKV_GEMM, st, [&] {
              return check_hip(kvp::gemm_f32((const float*)io.a, wr, M, N, h, proj, nullptr, st),
                               "projection GEMM (fp32)");
@@ -517,7 +517,9 @@ namespace {
 
 int round64(int S) { return (S + 63) / 64 * 64; }
 
-// Per-layer activations of kvp_train_forward, layer l at l * stride.
+// Per-layer activations of kvp_train_forward, layer l at l * stride: Q (after RoPE), the
+// attention output O and the layer input X in the model dtype, and (bf16 models) the
+// log-sum-exp of the scores, which fp32 models recompute.
 struct Saved {
     size_t q = 0, o = 0, x = 0, lse = 0, stride = 0, total = 0;
 };
@@ -530,11 +532,11 @@ Saved saved_layout(const kvp_ctx& c, int B, int S) {
         off += align_up(bytes);
         return at;
     };
-    const size_t M = (size_t)B * S;
-    v.q = take(M * c.n_q() * 2);
-    v.o = take(M * c.n_q() * 2);
-    v.x = take(M * c.d.h * 2);
-    v.lse = take((size_t)B * c.d.a * round64(S) * sizeof(float));
+    const size_t M = (size_t)B * S, e = c.esize();
+    v.q = take(M * c.n_q() * e);
+    v.o = take(M * c.n_q() * e);
+    v.x = take(M * c.d.h * e);
+    if (c.bf16()) v.lse = take((size_t)B * c.d.a * round64(S) * sizeof(float));
     v.stride = off;
     v.total = off * c.d.L;
     return v;
@@ -542,7 +544,7 @@ Saved saved_layout(const kvp_ctx& c, int B, int S) {
 
 // Workspace of kvp_backward.
 struct BwdWs {
-    size_t gb = 0, dO = 0, dsum = 0, dqkv = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
+    size_t gb = 0, dO = 0, lse = 0, dsum = 0, dqkv = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
     size_t acc_plane = 0;          // floats of one dK or dV sum
     std::vector<int> acc_slot;     // per layer: index of its fp32 sum pair, or -1
 };
@@ -557,10 +559,6 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
     };
     const size_t M = (size_t)B * S;
     const size_t h = c.d.h, nq = c.n_q(), nkv = c.n_kv(), np = nq + 2 * nkv;
-    w.gb = take(M * h * 2);
-    w.dO = take(M * nq * 2);
-    w.dsum = take((size_t)B * c.d.a * round64(S) * sizeof(float));
-    w.dqkv = take(M * np * 2);
     // One fp32 dK/dV pair per producer that has consumers.
     w.acc_slot.assign(c.d.L, -1);
     int nacc = 0;
@@ -571,7 +569,22 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
                     w.acc_slot[l] = nacc++;
                     break;
                 }
-    w.acc_plane = (size_t)B * c.d.g * S * 128;
+    w.acc_plane = (size_t)B * c.d.g * S * c.d.d_h;
+    if (!c.bf16()) {
+        // fp32: dO, [dQ | dK | dV], the per-(token, head) log-sum-exp and D, the sums, RoPE.
+        w.dO = take(M * nq * sizeof(float));
+        w.dqkv = take(M * np * sizeof(float));
+        w.lse = take(M * c.d.a * sizeof(float));
+        w.dsum = take(M * c.d.a * sizeof(float));
+        w.acc = take((size_t)nacc * 2 * w.acc_plane * sizeof(float));
+        w.rope = take((size_t)S * (c.d.d_h / 2) * sizeof(float2));
+        w.total = off;
+        return w;
+    }
+    w.gb = take(M * h * 2);
+    w.dO = take(M * nq * 2);
+    w.dsum = take((size_t)B * c.d.a * round64(S) * sizeof(float));
+    w.dqkv = take(M * np * 2);
     w.acc = take((size_t)nacc * 2 * w.acc_plane * sizeof(float));
     w.wot = take(nq * h * 2);   // W_O^T [a*d_h][h]
     w.wst = take(h * np * 2);   // [W_Q; W_K; W_V]^T [h][np]
@@ -598,7 +611,6 @@ extern "C" int kvp_workspace_size(const kvp_ctx* ctx, int phase, int B, int S, s
     if (seq && S > ctx->d.max_seq)
         return fail(KVP_E_CAPACITY, "kvp_workspace_size: S > max_seq");
     if (phase == KVP_PHASE_BACKWARD) {
-        if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_workspace_size: the backward needs a bf16 model");
         *bytes = bwd_layout(*ctx, B, S).total;
         return ok();
     }
@@ -705,7 +717,6 @@ extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_d
 
 extern "C" int kvp_train_saved_size(const kvp_ctx* ctx, int B, int S, size_t* bytes) {
     if (!ctx || !bytes) return fail(KVP_E_INVALID_ARG, "kvp_train_saved_size: NULL argument");
-    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_train_saved_size: training needs a bf16 model");
     if (B < 1 || S < 1) return fail(KVP_E_INVALID_ARG, "kvp_train_saved_size: B and S must be >= 1");
     if (B > ctx->d.max_batch || S > ctx->d.max_seq)
         return fail(KVP_E_CAPACITY, "kvp_train_saved_size: B or S beyond max_batch / max_seq");
@@ -718,7 +729,6 @@ extern "C" int kvp_train_forward(kvp_ctx* ctx, const void* x, void* y, int B, in
     Workspace w;
     int rc = check_prefill_args(ctx, x, y, B, S, ws, ws_bytes, &w);
     if (rc) return rc;
-    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_train_forward: training needs a bf16 model");
     const Saved sv = saved_layout(*ctx, B, S);
     if (!saved || saved_bytes < sv.total || !aligned16(saved))
         return fail(KVP_E_WORKSPACE, "kvp_train_forward: saved buffer needs %zu bytes (16-byte aligned), got %zu",
@@ -727,23 +737,34 @@ extern "C" int kvp_train_forward(kvp_ctx* ctx, const void* x, void* y, int B, in
     hipStream_t st = (hipStream_t)stream;
     char* base = (char*)ws;
     char* sb = (char*)saved;
-    if ((rc = timed(ctx, KVP_K_ROPE_TABLE, st, [&] {
-             return check_hip(kvp::rope_table((float2*)(base + w.rope), S, ctx->d.d_h, ctx->d.rope_base, st),
-                              "RoPE table");
-         })))
+    const bool bf = ctx->bf16();
+    if (bf && (rc = timed(ctx, KVP_K_ROPE_TABLE, st, [&] {
+                   return check_hip(kvp::rope_table((float2*)(base + w.rope), S, ctx->d.d_h, ctx->d.rope_base,
+                                                    st),
+                                    "RoPE table");
+               })))
         return rc;
     const int L = ctx->d.L;
     float* xr = (float*)(base + w.xr);
     for (int l = 0; l < L; ++l) {
         char* lay = sb + (size_t)l * sv.stride;
+        void* next_x = l == L - 1 ? y : (void*)(sb + (size_t)(l + 1) * sv.stride + sv.x);
         LayerIO io;
         io.a = l == 0 ? x : (const void*)(lay + sv.x);
-        io.res = l == 0 ? x : (const void*)xr;
-        io.res_f32 = l != 0;
-        io.y = l == L - 1 ? y : (void*)(sb + (size_t)(l + 1) * sv.stride + sv.x);
-        io.yf = l == L - 1 ? nullptr : xr;
+        if (bf) {
+            // The bf16 copy of the layer input is saved; the fp32 stream stays in xr.
+            io.res = l == 0 ? x : (const void*)xr;
+            io.res_f32 = l != 0;
+            io.yf = l == L - 1 ? nullptr : xr;
+        } else {
+            // fp32: the stream itself moves from one layer's saved input to the next.
+            io.res = io.a;
+            io.res_f32 = true;
+            io.yf = nullptr;
+        }
+        io.y = next_x;
         if ((rc = run_prefill_layer(ctx, l, io, lay + sv.o, base, w, B, S, st, lay + sv.q,
-                                    (float*)(lay + sv.lse))))
+                                    bf ? (float*)(lay + sv.lse) : nullptr)))
             return rc;
     }
     return ok();
@@ -769,11 +790,109 @@ extern "C" int kvp_set_layer_grads(kvp_ctx* ctx, int l, void* dWq, void* dWk, vo
     return ok();
 }
 
+namespace {
+
+// Backward of an fp32 model: the same sequence as the bf16 path, every product on the
+// vector ALUs in fp32.  G, the gradient at the current layer's output, is dY for the
+// last layer and dX (updated in place, after its last read) below it.
+int backward_f32(kvp_ctx* ctx, const float* x, const float* dy, float* dx, int B, int S, const Saved& sv,
+                 const char* sb, const BwdWs& w, char* base, hipStream_t st) {
+    const int h = ctx->d.h, nq = ctx->n_q(), nkv = ctx->n_kv(), L = ctx->d.L, M = B * S;
+    float* dO = (float*)(base + w.dO);
+    float* dqkv = (float*)(base + w.dqkv);
+    float* acc = (float*)(base + w.acc);
+    float2* rope = (float2*)(base + w.rope);
+    auto gemm = [&](auto&& f) { return timed(ctx, KVP_K_BWD_GEMM, st, f); };
+    int rc;
+    if ((rc = timed(ctx, KVP_K_BWD_AUX, st, [&] {
+             return check_hip(kvp::rope_table(rope, S, ctx->d.d_h, ctx->d.rope_base, st), "RoPE table");
+         })))
+        return rc;
+    std::vector<char> acc_written(L, 0);
+    for (int l = L - 1; l >= 0; --l) {
+        const int p = ctx->tau[l];
+        const bool producer = p == l;
+        const int np = producer ? nq + 2 * nkv : nq;
+        const Layer& Ly = ctx->layers[l];
+        const Layer& Pl = ctx->layers[p];
+        const char* lay = sb + (size_t)l * sv.stride;
+        const float* Ql = (const float*)(lay + sv.q);
+        const float* Ol = (const float*)(lay + sv.o);
+        const float* Xl = l == 0 ? x : (const float*)(lay + sv.x);
+        const float* G = l == L - 1 ? dy : dx;
+        // dO = G W_O, dW_O = G^T O.
+        if ((rc = gemm([&] {
+                 return check_hip(kvp::gemm_f32_strided(G, h, 1, (const float*)Ly.wo, nq, 1, nullptr, dO, nq, M,
+                                                        nq, h, st),
+                                  "dO GEMM (fp32)");
+             })))
+            return rc;
+        if ((rc = gemm([&] {
+                 return check_hip(kvp::gemm_f32_strided(G, 1, h, Ol, nq, 1, nullptr, Ly.dwo, nq, h, nq, M, st),
+                                  "dW_O GEMM (fp32)");
+             })))
+            return rc;
+        // Attention: dQ into dqkv; dK, dV into the producer's sums (consumer) or dqkv (producer).
+        kvp::AttnBwdF32 a{};
+        a.q = Ql; a.dO = dO; a.O = Ol; a.kc = (const float*)Pl.kc; a.vc = (const float*)Pl.vc; a.rope = rope;
+        a.lse = (float*)(base + w.lse);
+        a.dsum = (float*)(base + w.dsum);
+        const int slot = w.acc_slot[p];
+        float* ak = slot >= 0 ? acc + (size_t)slot * 2 * w.acc_plane : nullptr;
+        float* av = slot >= 0 ? ak + w.acc_plane : nullptr;
+        a.acc_in_k = acc_written[p] ? ak : nullptr;
+        a.acc_in_v = acc_written[p] ? av : nullptr;
+        if (!producer) {
+            a.acc_out_k = ak;
+            a.acc_out_v = av;
+            acc_written[p] = 1;
+        } else {
+            a.out_kv = dqkv;
+            a.col_k = nq;
+            a.col_v = nq + nkv;
+        }
+        a.out_q = dqkv;
+        a.ldo = np;
+        a.B = B; a.S = S; a.a = ctx->d.a; a.g = ctx->d.g; a.d = ctx->d.d_h; a.cap = ctx->d.kv_capacity;
+        if ((rc = timed(ctx, KVP_K_BWD_ATTN_KV, st, [&] {
+                 return check_hip(kvp::attn_bwd_f32(a, st), "attention backward (fp32)");
+             })))
+            return rc;
+        // dW_Q (, dW_K, dW_V) = [dQ | dK | dV]^T X_l; dX_l = G + dQ W_Q (+ dK W_K + dV W_V).
+        struct Part {
+            int col, rows;
+            const void* wt;
+            float* dw;
+        };
+        const Part parts[3] = {{0, nq, Ly.wq, Ly.dwq}, {nq, nkv, Ly.wk, Ly.dwk}, {nq + nkv, nkv, Ly.wv, Ly.dwv}};
+        for (int i = 0; i < (producer ? 3 : 1); ++i) {
+            const Part& pt = parts[i];
+            if ((rc = gemm([&] {
+                     return check_hip(kvp::gemm_f32_strided(dqkv + pt.col, 1, np, Xl, h, 1, nullptr, pt.dw, h,
+                                                            pt.rows, h, M, st),
+                                      "dW_QKV GEMM (fp32)");
+                 })))
+                return rc;
+        }
+        for (int i = 0; i < (producer ? 3 : 1); ++i) {
+            const Part& pt = parts[i];
+            if ((rc = gemm([&] {
+                     return check_hip(kvp::gemm_f32_strided(dqkv + pt.col, np, 1, (const float*)pt.wt, h, 1,
+                                                            i == 0 ? G : dx, dx, h, M, h, pt.rows, st),
+                                      "dX GEMM (fp32)");
+                 })))
+                return rc;
+        }
+    }
+    return ok();
+}
+
+}  // namespace
+
 extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* dx, int B, int S,
                             const void* saved, size_t saved_bytes, void* ws, size_t ws_bytes,
                             void* stream) {
     if (!ctx || !x || !dy || !dx) return fail(KVP_E_INVALID_ARG, "kvp_backward: NULL argument");
-    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_backward: training needs a bf16 model");
     if (dx == dy || dx == x) return fail(KVP_E_INVALID_ARG, "kvp_backward: dx must not alias dy or x");
     if (!aligned16(x) || !aligned16(dy) || !aligned16(dx))
         return fail(KVP_E_INVALID_ARG, "kvp_backward: x, dy, dx must be 16-byte aligned");
@@ -799,6 +918,9 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
             return fail(KVP_E_STATE, "kvp_backward: gradient buffers of layer %d were never set", l);
 
     hipStream_t st = (hipStream_t)stream;
+    if (!ctx->bf16())
+        return backward_f32(ctx, (const float*)x, (const float*)dy, (float*)dx, B, S, sv, (const char*)saved, w,
+                            (char*)ws, st);
     char* base = (char*)ws;
     const char* sb = (const char*)saved;
     auto bp = [&](size_t off) { return (uint16_t*)(base + off); };

@@ -298,14 +298,15 @@ def test_training_entry_points_host_checks():
         m.kvp_backward(16, 32, 48, 2, 200, 64, n1, 80, 16)
     assert e.value.code == kb.KVP_E_WORKSPACE
     m.close()
-    # fp32 models have no training path.
-    f = kb.Model(1, 64, 1, 1, 64, kb.KVP_DTYPE_FP32, [0], max_batch=1, max_seq=8, kv_capacity=8)
+    # fp32 models: Q, O, X [8][64] fp32 per layer, no saved log-sum-exp (it is recomputed).
+    f = kb.Model(2, 64, 1, 1, 64, kb.KVP_DTYPE_FP32, [0, 0], max_batch=1, max_seq=8, kv_capacity=8)
+    assert f.kvp_train_saved_size(1, 8) == 2 * 3 * 8 * 64 * 4
+    # dO, dQKV (producer width), statistics, one dK/dV sum pair, RoPE table; each
+    # piece rounded up to 256 bytes.
+    assert f.kvp_workspace_size(kb.KVP_PHASE_BACKWARD, 1, 8) == (2048 + 6144 + 256 + 256 + 4096 + 2048)
     with pytest.raises(kb.KvpError) as e:
-        f.kvp_train_saved_size(1, 8)
-    assert e.value.code == kb.KVP_E_SHAPE
-    with pytest.raises(kb.KvpError) as e:
-        f.kvp_workspace_size(kb.KVP_PHASE_BACKWARD, 1, 8)
-    assert e.value.code == kb.KVP_E_SHAPE
+        f.kvp_train_saved_size(1, 9)
+    assert e.value.code == kb.KVP_E_CAPACITY
     f.close()
 
 

@@ -1,7 +1,9 @@
 """GPU parity of the training path through the C ABI: kvp_train_forward (same output
 as kvp_prefill, plus saved activations) and kvp_backward against the fp64 backward
 oracle, on the same seeded inputs: dX and every weight gradient, with producers
-that have zero, one and two consumers, GQA ratios 1, 2 and 4, ragged S and S = 1."""
+that have zero, one and two consumers, GQA ratios 1, 2 and 4, ragged S and S = 1; bf16
+models at 2e-2 of max|ref| per tensor, fp32 models (the tiny fp32 configuration among
+them) at 1e-5."""
 import numpy as np
 import pytest
 import torch
@@ -11,8 +13,9 @@ from kvp_inputs import device as kd
 from oracle import backward as obw
 from paper_2608_15943_amd import binding as kb
 
-from gpu_util import (DEV, build_device_model, oracle_weights, rel_err, say, small_workload, to_np,
-                      workspace)
+from gpu_util import (DEV, build_device_model, oracle_weights, rel_err, say, small_workload, tdtype,
+                      to_np, workspace)
+from gpu_util import tol as tol_for
 
 pytestmark = pytest.mark.gpu
 
@@ -28,11 +31,12 @@ TOL = 2e-2   # bf16 path: max|err| <= 2e-2 max|ref| per tensor
 
 
 def _train_case(w, B, S, cap):
-    say(f"[backward] {w.name} B={B} S={S} tau={w.tau}")
+    say(f"[backward] {w.name} {w.dtype} B={B} S={S} tau={w.tau}")
+    tol = tol_for(w)
     dm = build_device_model(w, B, S, cap)
     m = dm.model
     st = torch.cuda.current_stream().cuda_stream
-    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device=DEV)
+    x = torch.empty((B, S, w.h), dtype=tdtype(w), device=DEV)
     kd.fill_prefill_x(w, x.data_ptr(), B, S)
     y = torch.empty_like(x)
     y_ref = torch.empty_like(x)
@@ -74,7 +78,7 @@ def _train_case(w, B, S, cap):
         e = rel_err(to_np(dx[b]), dxb)
         say(f"  dx[{b}]: {e:.3e}")
         worst = max(worst, e)
-        assert e <= TOL, ("dx", b, e)
+        assert e <= tol, ("dx", b, e)
         if ref_g is None:
             ref_g = gb
         else:
@@ -91,7 +95,7 @@ def _train_case(w, B, S, cap):
             got = to_np(grads[l][k])
             if S == 1 and k in ("dwq", "dwk"):
                 # One visible key: the softmax Jacobian is zero, so dQ = dK = 0 exactly;
-                # the bf16 path leaves a rounding residual of dP - D, bounded here by the
+                # the kernels may leave a rounding residual of dP - D, bounded here by the
                 # tolerance against the same attention's value-path gradient dW_V.
                 assert np.abs(ref_g[l][k]).max() < 1e-12
                 scale = np.abs(ref_g[p]["dwv"]).max()
@@ -100,7 +104,7 @@ def _train_case(w, B, S, cap):
                 e = rel_err(got, ref_g[l][k])
             say(f"  layer {l} {k}: {e:.3e}")
             worst = max(worst, e)
-            assert e <= TOL, (l, k, e)
+            assert e <= tol, (l, k, e)
     say(f"  max rel err {worst:.3e}")
 
 
@@ -115,6 +119,23 @@ def test_backward_matches_oracle(h, a, g, tau, B, S):
     w = small_workload(f"bwd-h{h}-a{a}-g{g}", len(tau), h, a, g, tau, seed=21)
     cap = (S + 63) // 64 * 64
     _train_case(w, B, S, cap)
+
+
+def test_backward_tiny_fp32_config():
+    """The tiny fp32 configuration (4 layers, d_model 256, 4 x 64 heads, S 128, map
+    [0, 0, 2, 2]) through the fp32 training path, at 1e-5."""
+    w = ki.tiny_fp32()
+    _train_case(w, w.batch, w.seq, w.kv_capacity)
+
+
+@pytest.mark.parametrize("h,a,g,d,tau,B,S", [
+    (128, 4, 2, 32, [0, 0, 2], 2, 37),       # GQA r = 2, ragged S, one consumer
+    (64, 4, 1, 16, [0, 0, 0], 1, 50),        # r = 4, two consumers of one producer
+    (128, 2, 2, 64, [0, 0], 2, 1),           # S = 1
+])
+def test_backward_fp32_matches_oracle(h, a, g, d, tau, B, S):
+    w = small_workload(f"bwd32-h{h}-a{a}-g{g}-d{d}", len(tau), h, a, g, tau, dtype="fp32", d_h=d, seed=23)
+    _train_case(w, B, S, S + 3)
 
 
 
