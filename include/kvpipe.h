@@ -323,6 +323,79 @@ int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max
                     int B, void* ws, size_t ws_bytes, void* stream);
 
 /* ======================================================================== */
+/* Paged KV storage (capacity-driven serving)                                 */
+/* ======================================================================== */
+/*
+ * Sec. 1 and Sec. 4 credit KV sharing, at inference, with a smaller KV cache and
+ * hence larger batches.  Contiguous slots reserve kv_capacity positions for every
+ * sequence; paged storage holds each sequence's positions in 64-position pages
+ * drawn from one pool per producer, so a fixed amount of HBM holds as many tokens
+ * as the pools have pages, whatever the mix of lengths, and a consumer layer adds
+ * no pages.
+ *
+ * Page layout (bf16 models): producer l's pool K [n_pages][g][64][d_h] and
+ * V [n_pages][g][d_h][64] (V transposed within the page, as in the slots).  A
+ * device page table pages [B][stride] (int32, row b for sequence b of the call)
+ * maps position p of sequence b to page pages[b][p / 64], row p % 64, in every
+ * producer's pool.  Entries are clamped to [0, n_pages) on the device, so a bad
+ * entry reads or writes a wrong page of the pool but never leaves it; entries
+ * covering positions a call touches must be mapped (kvp_pager_*).
+ */
+
+/* kvp_set_kv_pool -- producer l's page pools (device, caller-owned, 16-byte
+ * aligned), n_pages pages each.  Consumers have none; they read tau(l)'s.
+ * Errors: KVP_E_INVALID_ARG (NULL pool, n_pages < 1, l not a producer),
+ * KVP_E_SHAPE (fp32 model). */
+int kvp_set_kv_pool(kvp_ctx* ctx, int l, void* K, void* V, int n_pages);
+
+/* kvp_page_bytes -- bytes of one page (K and V) in one producer's pool:
+ * 2 * 64 * g * d_h * sizeof(dtype).  A budget of H bytes holds
+ * H / (bytes * number of producers) pages.  Errors: KVP_E_INVALID_ARG. */
+int kvp_page_bytes(const kvp_ctx* ctx, size_t* bytes);
+
+/*
+ * kvp_prefill_paged -- kvp_prefill with the producers' K/V written to and read
+ * from the pools: positions [0, S) of sequence b go to the pages of row b of
+ * `pages` (device int32 [B][pages_stride]).  Same kernels and arithmetic as
+ * kvp_prefill: y is bit-identical and the pages hold the values the slots would.
+ * Errors: as kvp_prefill, plus KVP_E_CAPACITY (S > 64 * pages_stride),
+ * KVP_E_STATE (a pool never set), KVP_E_SHAPE (fp32 model).
+ */
+int kvp_prefill_paged(kvp_ctx* ctx, const void* x, void* y, int B, int S, const int32_t* pages,
+                      int pages_stride, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * kvp_decode_step_paged -- kvp_decode_step over the pools: every producer
+ * appends at position len_b of row b of `pages`, and every layer attends over
+ * positions [0, len_b] through it.  Same kernels and arithmetic as
+ * kvp_decode_step (bit-identical y).  Errors: as kvp_decode_step, with
+ * KVP_E_CAPACITY when max_len >= 64 * pages_stride; KVP_E_STATE, KVP_E_SHAPE.
+ */
+int kvp_decode_step_paged(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
+                          const int32_t* pages, int pages_stride, void* y, int B, void* ws,
+                          size_t ws_bytes, void* stream);
+
+/*
+ * Host page allocator.  One table of max_seqs rows x max_pages_per_seq entries
+ * (-1 = unmapped) over n_pages pages; free pages are handed out lowest first
+ * from a fresh pager, and a released sequence's pages are reused first.
+ *   kvp_pager_reserve  -- grow sequence seq to hold positions [0, n_tokens);
+ *                         all or nothing: KVP_E_CAPACITY when the pool or the
+ *                         row is too small (nothing changes); never shrinks.
+ *   kvp_pager_release  -- return all of seq's pages.
+ *   kvp_pager_rows     -- copy the rows of seqs[0..B) to out [B][max_pages_per_seq]
+ *                         (host memory; the caller copies it to the device).
+ * Host memory only; not thread-safe (one pager per thread).
+ */
+typedef struct kvp_pager kvp_pager;
+int kvp_pager_create(int n_pages, int max_seqs, int max_pages_per_seq, kvp_pager** out);
+void kvp_pager_destroy(kvp_pager* p);
+int kvp_pager_reserve(kvp_pager* p, int seq, int n_tokens);
+int kvp_pager_release(kvp_pager* p, int seq);
+int kvp_pager_free_pages(const kvp_pager* p, int* n);
+int kvp_pager_rows(const kvp_pager* p, const int32_t* seqs, int B, int32_t* out);
+
+/* ======================================================================== */
 /* Training: forward that keeps activations, and the backward pass           */
 /* ======================================================================== */
 /*

@@ -10,6 +10,8 @@ from __future__ import annotations
 
 import ctypes as C
 import os
+
+import numpy as np
 from typing import Optional, Sequence
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -42,6 +44,9 @@ EXPORTS = [
     "kvp_prefill", "kvp_layer_forward", "kvp_decode_step", "kvp_get_map", "kvp_status_string",
     "kvp_last_error", "kvp_profile_enable", "kvp_profile_read",
     "kvp_train_saved_size", "kvp_train_forward", "kvp_set_layer_grads", "kvp_backward",
+    "kvp_set_kv_pool", "kvp_page_bytes", "kvp_prefill_paged", "kvp_decode_step_paged",
+    "kvp_pager_create", "kvp_pager_destroy", "kvp_pager_reserve", "kvp_pager_release",
+    "kvp_pager_free_pages", "kvp_pager_rows",
     # include/kvp_calib.h: achievable-peak calibration (measurement support)
     "kvp_calib_mfma_bf16", "kvp_calib_stream_read",
 ]
@@ -116,6 +121,16 @@ def lib() -> C.CDLL:
         "kvp_train_forward": ([vp, vp, vp, i32, i32, vp, C.c_size_t, vp, C.c_size_t, vp], i32),
         "kvp_set_layer_grads": ([vp, i32, vp, vp, vp, vp], i32),
         "kvp_backward": ([vp, vp, vp, vp, i32, i32, vp, C.c_size_t, vp, C.c_size_t, vp], i32),
+        "kvp_set_kv_pool": ([vp, i32, vp, vp, i32], i32),
+        "kvp_page_bytes": ([vp, C.POINTER(C.c_size_t)], i32),
+        "kvp_prefill_paged": ([vp, vp, vp, i32, i32, vp, i32, vp, C.c_size_t, vp], i32),
+        "kvp_decode_step_paged": ([vp, vp, vp, i32, vp, i32, vp, i32, vp, C.c_size_t, vp], i32),
+        "kvp_pager_create": ([i32, i32, i32, C.POINTER(vp)], i32),
+        "kvp_pager_destroy": ([vp], None),
+        "kvp_pager_reserve": ([vp, i32, i32], i32),
+        "kvp_pager_release": ([vp, i32], i32),
+        "kvp_pager_free_pages": ([vp, C.POINTER(i32)], i32),
+        "kvp_pager_rows": ([vp, C.POINTER(C.c_int32), i32, C.POINTER(C.c_int32)], i32),
         "kvp_status_string": ([i32], C.c_char_p),
         "kvp_last_error": ([], C.c_char_p),
         "kvp_profile_enable": ([vp, i32], i32),
@@ -286,6 +301,23 @@ class Model:
         _check(lib().kvp_decode_step(self.ctx, x, len_dev, max_len, y, B, ws, ws_bytes,
                                      stream or None), "kvp_decode_step")
 
+    def kvp_set_kv_pool(self, l, k, v, n_pages):
+        _check(lib().kvp_set_kv_pool(self.ctx, l, k, v, n_pages), "kvp_set_kv_pool")
+
+    def kvp_page_bytes(self) -> int:
+        n = C.c_size_t()
+        _check(lib().kvp_page_bytes(self.ctx, C.byref(n)), "kvp_page_bytes")
+        return n.value
+
+    def kvp_prefill_paged(self, x, y, B, S, pages_dev, pages_stride, ws, ws_bytes, stream=0):
+        _check(lib().kvp_prefill_paged(self.ctx, x, y, B, S, pages_dev, pages_stride, ws, ws_bytes,
+                                       stream or None), "kvp_prefill_paged")
+
+    def kvp_decode_step_paged(self, x, len_dev, max_len, pages_dev, pages_stride, y, B, ws, ws_bytes,
+                              stream=0):
+        _check(lib().kvp_decode_step_paged(self.ctx, x, len_dev, max_len, pages_dev, pages_stride, y, B,
+                                           ws, ws_bytes, stream or None), "kvp_decode_step_paged")
+
     def kvp_profile_enable(self, enable=True):
         _check(lib().kvp_profile_enable(self.ctx, 1 if enable else 0), "kvp_profile_enable")
 
@@ -317,3 +349,51 @@ def kvp_calib_stream_read(src: int, nbytes: int, sink: int, stream: int = 0) -> 
     """Launch the streaming read of nbytes at device address src."""
     _check(lib().kvp_calib_stream_read(C.c_void_p(src), C.c_size_t(nbytes), C.c_void_p(sink),
                                        C.c_void_p(stream)), "kvp_calib_stream_read")
+
+
+class Pager:
+    """Host page allocator (kvp_pager_*): a table of max_seqs rows x max_pages entries."""
+
+    def __init__(self, n_pages, max_seqs, max_pages):
+        p = C.c_void_p()
+        _check(lib().kvp_pager_create(n_pages, max_seqs, max_pages, C.byref(p)), "kvp_pager_create")
+        self.p = p
+        self.max_pages = max_pages
+
+    def close(self):
+        if self.p:
+            lib().kvp_pager_destroy(self.p)
+            self.p = C.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def reserve(self, seq, n_tokens):
+        _check(lib().kvp_pager_reserve(self.p, seq, n_tokens), "kvp_pager_reserve")
+
+    def try_reserve(self, seq, n_tokens) -> bool:
+        """reserve(); False (and nothing reserved) when the pool or the row is too small."""
+        rc = lib().kvp_pager_reserve(self.p, seq, n_tokens)
+        if rc == KVP_E_CAPACITY:
+            return False
+        _check(rc, "kvp_pager_reserve")
+        return True
+
+    def release(self, seq):
+        _check(lib().kvp_pager_release(self.p, seq), "kvp_pager_release")
+
+    def free_pages(self) -> int:
+        n = C.c_int()
+        _check(lib().kvp_pager_free_pages(self.p, C.byref(n)), "kvp_pager_free_pages")
+        return n.value
+
+    def rows(self, seqs):
+        """Host table rows of seqs: numpy int32 [len(seqs)][max_pages], -1 where unmapped."""
+        seqs = np.ascontiguousarray(seqs, dtype=np.int32)
+        out = np.empty((len(seqs), self.max_pages), dtype=np.int32)
+        _check(lib().kvp_pager_rows(self.p, seqs.ctypes.data_as(C.POINTER(C.c_int32)), len(seqs),
+                                    out.ctypes.data_as(C.POINTER(C.c_int32))), "kvp_pager_rows")
+        return out

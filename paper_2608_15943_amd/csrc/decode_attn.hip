@@ -58,10 +58,12 @@ __device__ __forceinline__ SeqTiles seq_tiles(const int32_t* lens, int B, int ca
 }
 
 // One wave per workgroup, one workgroup per SIMD (the grid is sized to the device).
+// PAGED: every 64-position tile is one page, looked up once per tile.
+template <bool PAGED>
 __global__ __launch_bounds__(64, 1) void decode_attn_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     const int32_t* __restrict__ lens, float* __restrict__ part, int B, int a, int g, int cap,
-    float scale_log2) {
+    float scale_log2, Pages pages) {
     const int lane = threadIdx.x;
     const int W = gridDim.x, w = blockIdx.x;
     const int r = a / g;
@@ -94,10 +96,22 @@ __global__ __launch_bounds__(64, 1) void decode_attn_kernel(
 
     // Position held by MFMA row rho (= lane & 15 for the A operand) of score block tb
     // of a tile: block 2s + e covers positions 32 s + 8 (rho / 4) + 4 e + rho % 4.
-    // Tiles start at multiples of 64 and cap % 64 == 0, so every load stays in the slot.
+    // Tiles start at multiples of 64 and cap % 64 == 0, so every load stays in the slot
+    // (or, paged, in the tile's page).
     auto load = [&](int lb, int lh, int t0, DTile& tl) {
-        const uint16_t* kbase = Kc + ((size_t)lb * g + lh) * cap * D;
-        const uint16_t* vbase = Vc + ((size_t)lb * g + lh) * D * cap;
+        const uint16_t* kbase;
+        const uint16_t* vbase;
+        int vld;
+        if constexpr (PAGED) {
+            const int pg = page_at(pages, lb, t0 / TILE);
+            kbase = Kc + ((size_t)pg * g + lh) * TILE * D - (size_t)t0 * D;
+            vbase = Vc + ((size_t)pg * g + lh) * D * TILE - t0;
+            vld = TILE;
+        } else {
+            kbase = Kc + ((size_t)lb * g + lh) * cap * D;
+            vbase = Vc + ((size_t)lb * g + lh) * D * cap;
+            vld = cap;
+        }
 #pragma unroll
         for (int tb = 0; tb < 4; ++tb) {
             const int s = tb >> 1, e = tb & 1;
@@ -108,7 +122,7 @@ __global__ __launch_bounds__(64, 1) void decode_attn_kernel(
         }
 #pragma unroll
         for (int db = 0; db < 8; ++db) {
-            const uint16_t* vr = vbase + (size_t)(16 * db + col) * cap + t0 + 8 * grp;
+            const uint16_t* vr = vbase + (size_t)(16 * db + col) * vld + t0 + 8 * grp;
 #pragma unroll
             for (int s = 0; s < 2; ++s) tl.v[db][s] = *(const u32x4*)(vr + 32 * s);
         }
@@ -299,11 +313,17 @@ __global__ __launch_bounds__(kCombineThreads) void decode_combine_kernel(
 
 hipError_t decode_attn_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                             const int32_t* lens, float* part, int B, int a, int g, int cap, int waves,
-                            hipStream_t st) {
+                            const Pages& pages, hipStream_t st) {
     if (B < 1 || B > 64 || waves < 1 || waves > kMaxDecodeSplits) return hipErrorInvalidValue;
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-    hipLaunchKernelGGL(decode_attn_kernel, dim3(waves), dim3(64), 0, st, q, kc, vc, lens, part, B, a, g,
-                       cap, scale_log2);
+    if (pages.pt) {
+        if (pages.n < 1 || pages.stride < 1 || cap != TILE * pages.stride) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(decode_attn_kernel<true>, dim3(waves), dim3(64), 0, st, q, kc, vc, lens, part, B, a,
+                           g, cap, scale_log2, pages);
+    } else {
+        hipLaunchKernelGGL(decode_attn_kernel<false>, dim3(waves), dim3(64), 0, st, q, kc, vc, lens, part, B,
+                           a, g, cap, scale_log2, pages);
+    }
     return hipGetLastError();
 }
 

@@ -162,18 +162,31 @@ __global__ __launch_bounds__(256) void decode_resid_kernel(const float* __restri
 }
 
 // Sum of the K slices of sequence b's projections, RoPE at position len_b, then
-// Q -> q [B][a * 128] (bf16), K -> K slot row len_b, V -> V^T slot column len_b.  Work
+// Q -> q [B][a * 128] (bf16), K -> K slot row len_b, V -> V^T slot column len_b (or the
+// row / column len_b % 64 of page len_b / 64 of sequence b when pages.pt is set).  Work
 // item j of a row: a rotary pair (head h < a + g_p, dim i < 64), then the V elements.
 __global__ __launch_bounds__(256) void decode_qkv_epi_kernel(const float* __restrict__ part, int nsplit,
                                                              int B, int N, const int32_t* __restrict__ lens,
                                                              int a, int g, int cap, double base,
                                                              int producer, uint16_t* __restrict__ q,
                                                              uint16_t* __restrict__ kc,
-                                                             uint16_t* __restrict__ vc) {
+                                                             uint16_t* __restrict__ vc, Pages pages) {
     constexpr int D = 128, HALF = 64;
     __shared__ float2 cs[HALF];
     const int b = blockIdx.y;
-    const int pos = max(0, min(lens[b], cap - 1));   // never outside the slot
+    const int pos = max(0, min(lens[b], cap - 1));   // never outside the slot (or page table row)
+    // Slot (b, kv head 0) base and the row of pos, in units of D elements.
+    size_t kv0;
+    int vld, row;
+    if (pages.pt) {
+        kv0 = (size_t)page_at(pages, b, pos / kPage) * g * kPage;
+        vld = kPage;
+        row = pos % kPage;
+    } else {
+        kv0 = (size_t)b * g * cap;
+        vld = cap;
+        row = pos;
+    }
     if (threadIdx.x < HALF) {
         const double theta = pow(base, -2.0 * threadIdx.x / D);
         double sd, cd;
@@ -202,13 +215,13 @@ __global__ __launch_bounds__(256) void decode_qkv_epi_kernel(const float* __rest
             q[(size_t)b * a * D + h * D + i] = f2bf(o1);
             q[(size_t)b * a * D + h * D + i + HALF] = f2bf(o2);
         } else {
-            const size_t kb = (((size_t)b * g + (h - a)) * cap + pos) * D;
+            const size_t kb = (kv0 + (size_t)(h - a) * vld + row) * D;
             kc[kb + i] = f2bf(o1);
             kc[kb + i + HALF] = f2bf(o2);
         }
     } else {
         const int e = j - npairs, h = e / D, c = e - h * D;
-        vc[(((size_t)b * g + h) * D + c) * cap + pos] = f2bf(val(a * D + g * D + e));
+        vc[(kv0 + (size_t)h * vld) * D + (size_t)c * vld + row] = f2bf(val(a * D + g * D + e));
     }
 }
 
@@ -241,11 +254,12 @@ hipError_t decode_resid_bf16(const float* part, int nsplit, int M, int N, const 
 
 hipError_t decode_qkv_epilogue_bf16(const float* part, int nsplit, int B, int N, const int32_t* lens, int a,
                                     int g, int cap, double base, bool producer, uint16_t* q, uint16_t* kc,
-                                    uint16_t* vc, hipStream_t st) {
+                                    uint16_t* vc, const Pages& pages, hipStream_t st) {
     if (nsplit < 1) return hipErrorInvalidValue;
+    if (pages.pt && (pages.n < 1 || pages.stride < 1 || cap != kPage * pages.stride)) return hipErrorInvalidValue;
     const int items = (a + (producer ? g : 0)) * 64 + (producer ? g * 128 : 0);
     hipLaunchKernelGGL(decode_qkv_epi_kernel, dim3((items + 255) / 256, B), dim3(256), 0, st, part, nsplit,
-                       B, N, lens, a, g, cap, base, producer ? 1 : 0, q, kc, vc);
+                       B, N, lens, a, g, cap, base, producer ? 1 : 0, q, kc, vc, pages);
     return hipGetLastError();
 }
 

@@ -4,7 +4,9 @@
 // which the backward rebuilds the softmax weights.
 //
 // A consumer layer runs the same kernel on its producer's slot (Eq. 3); the
-// kernel only sees a K slot and a V slot.
+// kernel only sees a K slot and a V slot (or, paged, the pools and the sequence's
+// page table row: a 128-position tile spans two 64-position pages, looked up once
+// per tile).
 //
 // Workgroup = 8 waves = 256 queries of one (sequence, head); wave w owns 32
 // queries; two waves per SIMD.  Keys and values stream through LDS in tiles of
@@ -65,10 +67,11 @@ __device__ __forceinline__ void load_lds_1k(const void* gsrc, void* lds_base) {
 __device__ __forceinline__ int swap_b23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
 // 8 waves of 32 queries; two waves per SIMD (<= 256 registers each), 128 KB of LDS.
+template <bool PAGED>
 __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
     uint16_t* __restrict__ O, float* __restrict__ lse, int Sp, int B, int S, int a, int g, int cap,
-    float scale_log2) {
+    float scale_log2, Pages pages) {
     // K: [stage][row * 16 + (chunk ^ (row & 15))]; V^T: [stage][d * 16 + (chunk ^ (d & 15))]
     // (rows of 256 bytes: 128 dims of a position, or 128 positions of a dim).
     __shared__ u32x4 lk[2][BKV * 16];
@@ -123,8 +126,33 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     // 16 wave + 4 j + lane / 16, four 256-byte rows per instruction.  Positions past the
     // slot (only in the last tile when cap % 128 == 64) are clamped to the slot's last
     // row / chunk: they lie beyond S, so their scores are masked and their V is zeroed.
+    // Paged, positions are clamped to the last one before S (whose page is mapped).
     auto issue_tile = [&](int t, int stg) {
         const int t0 = t * BKV;
+        if constexpr (PAGED) {
+            const int last = S - 1, vlast = last & ~7;
+            const int p0 = t0 / kPage;
+            const uint16_t* kp[2];
+            const uint16_t* vp[2];
+#pragma unroll
+            for (int h = 0; h < 2; ++h) {
+                const int pg = page_at(pages, b, min(p0 + h, last / kPage));
+                kp[h] = Kc + ((size_t)pg * g + kvh) * kPage * D;
+                vp[h] = Vc + ((size_t)pg * g + kvh) * D * kPage;
+            }
+#pragma unroll
+            for (int j = 0; j < 4; ++j) {
+                const int r = 16 * wave + 4 * j + (lane >> 4);
+                const int c = (lane & 15) ^ (r & 15);
+                const int pk = min(t0 + r, last);
+                load_lds_1k(kp[pk / kPage - p0] + (size_t)(pk % kPage) * D + 8 * c,
+                            &lk[stg][(16 * wave + 4 * j) * 16]);
+                const int pv = min(t0 + 8 * c, vlast);
+                load_lds_1k(vp[pv / kPage - p0] + (size_t)r * kPage + pv % kPage,
+                            &lv[stg][(16 * wave + 4 * j) * 16]);
+            }
+            return;
+        }
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
             const int r = 16 * wave + 4 * j + (lane >> 4);
@@ -297,11 +325,17 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
 
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                               uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
-                              hipStream_t st) {
+                              const Pages& pages, hipStream_t st) {
     const int nqt = (S + BQ - 1) / BQ;
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
-    hipLaunchKernelGGL(flash_prefill_kernel, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, lse, Sp,
-                       B, S, a, g, cap, scale_log2);
+    if (pages.pt) {
+        if (pages.n < 1 || pages.stride < 1 || S > kPage * pages.stride) return hipErrorInvalidValue;
+        hipLaunchKernelGGL(flash_prefill_kernel<true>, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, lse,
+                           Sp, B, S, a, g, cap, scale_log2, pages);
+    } else {
+        hipLaunchKernelGGL(flash_prefill_kernel<false>, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, lse,
+                           Sp, B, S, a, g, cap, scale_log2, pages);
+    }
     return hipGetLastError();
 }
 

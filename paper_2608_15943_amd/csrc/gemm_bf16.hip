@@ -68,6 +68,18 @@ struct QkvEpi {
     };
     QkvOut o;
     __device__ __forceinline__ void set_split(int) {}
+    // Element offsets of K row s and of V^T element (dimension n, position s) of
+    // sequence b, KV head `head`: in the contiguous slot or in s's page.
+    __device__ __forceinline__ size_t k_row(int b, int head, int s) const {
+        if (o.pages.pt)
+            return (((size_t)page_at(o.pages, b, s / kPage) * o.g + head) * kPage + s % kPage) * 128;
+        return (((size_t)b * o.g + head) * o.cap + s) * 128;
+    }
+    __device__ __forceinline__ size_t v_at(int b, int head, int n, int s) const {
+        if (o.pages.pt)
+            return (((size_t)page_at(o.pages, b, s / kPage) * o.g + head) * 128 + n) * kPage + s % kPage;
+        return (((size_t)b * o.g + head) * 128 + n) * o.cap + s;
+    }
     // Region of the wave's 128 columns: 0 = Q, 1 = K, 2 = V, -1 = past N.
     __device__ __forceinline__ int region(int nw, int N, int* head) const {
         if (nw >= N) return -1;
@@ -143,15 +155,14 @@ struct QkvEpi {
                 const u32x2 up = *(const u32x2*)(st + n * 256 + (((2 * k + 1) ^ sw) * 8));
                 const int b = m / o.S, s = m - b * o.S;
                 if (fast && m + 7 < M) {
-                    *(u32x4*)(o.vc + (((size_t)b * o.g + head) * 128 + n) * o.cap + s) =
-                        u32x4{lo[0], lo[1], up[0], up[1]};
+                    // s % 8 == 0: the 8 positions never straddle a 64-position page.
+                    *(u32x4*)(o.vc + v_at(b, head, n, s)) = u32x4{lo[0], lo[1], up[0], up[1]};
                 } else {
                     const uint32_t w4[4] = {lo[0], lo[1], up[0], up[1]};
                     for (int e = 0; e < 8 && m + e < M; ++e) {
                         int bb = b, ss = s + e;
                         while (ss >= o.S) { ss -= o.S; ++bb; }
-                        o.vc[(((size_t)bb * o.g + head) * 128 + n) * o.cap + ss] =
-                            (bf16_t)(w4[e >> 1] >> (16 * (e & 1)));
+                        o.vc[v_at(bb, head, n, ss)] = (bf16_t)(w4[e >> 1] >> (16 * (e & 1)));
                     }
                 }
             }
@@ -193,7 +204,7 @@ struct QkvEpi {
                 dst = o.q + (size_t)m * o.n_q + head * 128;
             } else {
                 const int b = m / o.S;
-                dst = o.kc + (((size_t)b * o.g + head) * o.cap + (m - b * o.S)) * 128;
+                dst = o.kc + k_row(b, head, m - b * o.S);
             }
             *(u32x4*)(dst + c0) = lo;
             *(u32x4*)(dst + c0 + 64) = up;

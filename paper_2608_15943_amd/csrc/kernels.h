@@ -14,6 +14,18 @@ struct WRows {
     int rows[3];
 };
 
+// KV storage.  Contiguous slots (pt == nullptr): K [B][g][cap][d], V [B][g][d][cap].
+// Paged: position p of sequence b lives in page pt[b * stride + p / kPage], row p % kPage,
+// of the pools K [n][g][kPage][d] and V [n][g][d][kPage]; entries are clamped to [0, n).
+constexpr int kPage = 64;
+struct Pages {
+    const int32_t* pt;
+    int stride, n;
+};
+__device__ __forceinline__ int page_at(const Pages& pg, int b, int j) {
+    return min(max(pg.pt[(size_t)b * pg.stride + j], 0), pg.n - 1);
+}
+
 // ---- bf16 prefill ---------------------------------------------------------
 
 // Q (all layers) and K, V (producers) projections with RoPE fused into the
@@ -25,6 +37,7 @@ struct QkvOut {
     uint16_t* vc;         // V slot [Bmax][g][128][cap] or nullptr
     const float2* rope;   // [S][64] (cos, sin)
     int n_q, n_kv, g, cap, S;
+    Pages pages;          // pages.pt != nullptr: kc, vc are page pools
 };
 hipError_t gemm_qkv_bf16(const uint16_t* x, const WRows& w, int M, int N, int K, const QkvOut& o,
                          hipStream_t st);
@@ -34,11 +47,12 @@ hipError_t gemm_qkv_bf16(const uint16_t* x, const WRows& w, int M, int N, int K,
 hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_res, bool x_f32,
                            uint16_t* y, float* yf, int M, int N, int K, hipStream_t st);
 
-// Causal flash attention: q [B*S][a*128], K/V slots of the producer, o [B*S][a*128];
-// lse (optional) [B][a][Sp]: the row log-sum-exp of the scaled scores, log2 domain.
+// Causal flash attention: q [B*S][a*128], K/V slots (or pools, pages.pt set) of the
+// producer, o [B*S][a*128]; lse (optional) [B][a][Sp]: the row log-sum-exp of the scaled
+// scores, log2 domain.
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                               uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
-                              hipStream_t st);
+                              const Pages& pages, hipStream_t st);
 
 // The slice count gemm_kmajor_out_bf16 should use for an M x N x K product.
 int gemm_out_splits(int M, int N, int K);
@@ -120,13 +134,14 @@ hipError_t decode_resid_bf16(const float* part, int nsplit, int M, int N, const 
 // column at position lens[b] of the slot.
 hipError_t decode_qkv_epilogue_bf16(const float* part, int nsplit, int B, int N, const int32_t* lens, int a,
                                     int g, int cap, double base, bool producer, uint16_t* q, uint16_t* kc,
-                                    uint16_t* vc, hipStream_t st);
+                                    uint16_t* vc, const Pages& pages, hipStream_t st);
 
 // Attention of one new query per sequence over positions [0, len_b], on a grid of
 // `waves` single-wave workgroups that split the (sequence, KV head, tile) list evenly.
+// Paged (pages.pt != nullptr): kc, vc are pools and cap = kPage * pages.stride.
 hipError_t decode_attn_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
                             const int32_t* lens, float* part, int B, int a, int g, int cap, int waves,
-                            hipStream_t st);
+                            const Pages& pages, hipStream_t st);
 hipError_t decode_combine_bf16(const float* part, const int32_t* lens, uint16_t* o, int B, int a, int g,
                                int cap, int waves, hipStream_t st);
 

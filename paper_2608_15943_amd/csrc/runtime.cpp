@@ -40,6 +40,9 @@ struct Layer {
     const void* wo = nullptr;
     void* kc = nullptr;
     void* vc = nullptr;
+    void* kp = nullptr;     // page pools (kvp_set_kv_pool)
+    void* vp = nullptr;
+    int n_pages = 0;
     bool weights = false;
     float* dwq = nullptr;   // weight gradients (training), fp32
     float* dwk = nullptr;
@@ -69,6 +72,13 @@ struct LayerIO {
     bool res_f32;      // res is fp32 (otherwise the model dtype)
     void* y;           // output [rows][h], model dtype
     float* yf;         // optional fp32 copy of the output (bf16 models)
+};
+
+// Device page table of a paged call: row b (stride entries) maps the 64-position pages of
+// sequence b to pages of every producer's pool.
+struct PageTable {
+    const int32_t* pt;
+    int stride;
 };
 
 }  // namespace
@@ -187,14 +197,28 @@ int timed(kvp_ctx* c, int kind, hipStream_t st, F&& launch) {
     return rc ? rc : rc2;
 }
 
-int check_layers(const kvp_ctx* c, int lo, int hi) {
+int check_layers(const kvp_ctx* c, int lo, int hi, bool paged = false) {
     for (int l = lo; l < hi; ++l) {
         if (!c->layers[l].weights) return fail(KVP_E_STATE, "weights of layer %d were never set", l);
         const int p = c->tau[l];
-        if (!c->layers[p].kc || !c->layers[p].vc)
-            return fail(KVP_E_STATE, "KV slot of producer %d (used by layer %d) was never set", p, l);
+        if (paged ? !c->layers[p].kp || !c->layers[p].vp : !c->layers[p].kc || !c->layers[p].vc)
+            return fail(KVP_E_STATE, "KV %s of producer %d (used by layer %d) was never set",
+                        paged ? "pool" : "slot", p, l);
     }
     return KVP_OK;
+}
+
+// Where producer P's K/V live for a call: its slot, or its pool under the page table.
+struct KvView {
+    void* k;
+    void* v;
+    int cap;
+    kvp::Pages pages;
+};
+
+KvView kv_view(const kvp_ctx* c, const Layer& P, const PageTable* pt) {
+    if (!pt) return {P.kc, P.vc, c->d.kv_capacity, kvp::Pages{nullptr, 0, 0}};
+    return {P.kp, P.vp, kvp::kPage * pt->stride, kvp::Pages{pt->pt, pt->stride, P.n_pages}};
 }
 
 kvp::WRows proj_rows(const kvp_ctx* c, int l, bool producer) {
@@ -215,10 +239,11 @@ kvp::WRows proj_rows(const kvp_ctx* c, int l, bool producer) {
 // (and io.yf), attention output into o_buf.
 int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* ws,
                       const Workspace& w, int B, int S, hipStream_t st, void* q_buf = nullptr,
-                      float* lse = nullptr) {
+                      float* lse = nullptr, const PageTable* pt = nullptr) {
     const int p = c->tau[l];
     const bool producer = p == l;
     const Layer& P = c->layers[p];
+    const KvView kv = kv_view(c, P, pt);
     const int M = B * S, h = c->d.h, nq = c->n_q();
     const int N = producer ? nq + 2 * c->n_kv() : nq;
     const kvp::WRows wr = proj_rows(c, l, producer);
@@ -229,24 +254,25 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
     if (c->bf16()) {
         kvp::QkvOut qo{};
         qo.q = (uint16_t*)(q_buf ? q_buf : ws + w.q);
-        qo.kc = producer ? (uint16_t*)P.kc : nullptr;
-        qo.vc = producer ? (uint16_t*)P.vc : nullptr;
+        qo.kc = producer ? (uint16_t*)kv.k : nullptr;
+        qo.vc = producer ? (uint16_t*)kv.v : nullptr;
         qo.rope = (const float2*)(ws + w.rope);
         qo.n_q = nq;
         qo.n_kv = producer ? c->n_kv() : 0;
         qo.g = c->d.g;
-        qo.cap = c->d.kv_capacity;
+        qo.cap = kv.cap;
         qo.S = S;
+        qo.pages = kv.pages;
         if ((rc = timed(c, KVP_K_QKV_GEMM, st, [&] {
                  return check_hip(kvp::gemm_qkv_bf16((const uint16_t*)io.a, wr, M, N, h, qo, st),
                                   "projection GEMM");
              })))
             return rc;
         if ((rc = timed(c, KVP_K_FLASH_ATTN, st, [&] {
-                 return check_hip(kvp::flash_prefill_bf16(qo.q, (const uint16_t*)P.kc,
-                                                          (const uint16_t*)P.vc, (uint16_t*)o_buf, lse,
+                 return check_hip(kvp::flash_prefill_bf16(qo.q, (const uint16_t*)kv.k,
+                                                          (const uint16_t*)kv.v, (uint16_t*)o_buf, lse,
                                                           (S + 63) / 64 * 64, B, S, c->d.a, c->d.g,
-                                                          c->d.kv_capacity, st),
+                                                          kv.cap, kv.pages, st),
                                   "flash attention");
              })))
             return rc;
@@ -287,10 +313,12 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
 }
 
 int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
-                     int max_len, char* ws, const Workspace& w, int B, hipStream_t st) {
+                     int max_len, char* ws, const Workspace& w, int B, hipStream_t st,
+                     const PageTable* pt = nullptr) {
     const int p = c->tau[l];
     const bool producer = p == l;
     const Layer& P = c->layers[p];
+    const KvView kv = kv_view(c, P, pt);
     const int h = c->d.h, nq = c->n_q();
     const int N = producer ? nq + 2 * c->n_kv() : nq;
     const kvp::WRows wr = proj_rows(c, l, producer);
@@ -313,10 +341,10 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
     if ((rc = timed(c, KVP_K_DEC_ROPE, st, [&] {
              return c->bf16()
                         ? check_hip(kvp::decode_qkv_epilogue_bf16(
-                                        proj, nsplit, B, N, lens, c->d.a, c->d.g, c->d.kv_capacity,
+                                        proj, nsplit, B, N, lens, c->d.a, c->d.g, kv.cap,
                                         c->d.rope_base, producer, (uint16_t*)q,
-                                        producer ? (uint16_t*)P.kc : nullptr,
-                                        producer ? (uint16_t*)P.vc : nullptr, st),
+                                        producer ? (uint16_t*)kv.k : nullptr,
+                                        producer ? (uint16_t*)kv.v : nullptr, kv.pages, st),
                                     "decode RoPE + cache append")
                         : check_hip(kvp::rope_scatter(proj, 1, 0, B, 0, lens, c->d.a, c->d.g, c->d.d_h,
                                                       c->d.kv_capacity, c->d.rope_base, producer, false,
@@ -328,15 +356,15 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
     if (c->bf16()) {
         float* part = (float*)(ws + w.part);
         if ((rc = timed(c, KVP_K_DEC_ATTN, st, [&] {
-                 return check_hip(kvp::decode_attn_bf16((const uint16_t*)q, (const uint16_t*)P.kc,
-                                                        (const uint16_t*)P.vc, lens, part, B, c->d.a,
-                                                        c->d.g, c->d.kv_capacity, c->decode_waves, st),
+                 return check_hip(kvp::decode_attn_bf16((const uint16_t*)q, (const uint16_t*)kv.k,
+                                                        (const uint16_t*)kv.v, lens, part, B, c->d.a,
+                                                        c->d.g, kv.cap, c->decode_waves, kv.pages, st),
                                   "decode attention");
              })))
             return rc;
         if ((rc = timed(c, KVP_K_DEC_COMBINE, st, [&] {
                  return check_hip(kvp::decode_combine_bf16(part, lens, (uint16_t*)o, B, c->d.a, c->d.g,
-                                                           c->d.kv_capacity, c->decode_waves, st),
+                                                           kv.cap, c->decode_waves, st),
                                   "decode combine");
              })))
             return rc;
@@ -511,6 +539,28 @@ extern "C" int kvp_set_kv_slot(kvp_ctx* ctx, int l, void* K, void* V) {
     return ok();
 }
 
+extern "C" int kvp_set_kv_pool(kvp_ctx* ctx, int l, void* K, void* V, int n_pages) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "kvp_set_kv_pool: NULL ctx");
+    if (l < 0 || l >= ctx->d.L) return fail(KVP_E_INVALID_ARG, "kvp_set_kv_pool: layer %d out of range", l);
+    if (ctx->tau[l] != l)
+        return fail(KVP_E_INVALID_ARG, "kvp_set_kv_pool: layer %d is a consumer and owns no pool", l);
+    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "kvp_set_kv_pool: paged KV storage needs a bf16 model");
+    if (!K || !V || n_pages < 1) return fail(KVP_E_INVALID_ARG, "kvp_set_kv_pool: NULL pool or n_pages < 1");
+    if (!aligned16(K) || !aligned16(V))
+        return fail(KVP_E_INVALID_ARG, "kvp_set_kv_pool: pools must be 16-byte aligned");
+    Layer& Ly = ctx->layers[l];
+    Ly.kp = K;
+    Ly.vp = V;
+    Ly.n_pages = n_pages;
+    return ok();
+}
+
+extern "C" int kvp_page_bytes(const kvp_ctx* ctx, size_t* bytes) {
+    if (!ctx || !bytes) return fail(KVP_E_INVALID_ARG, "kvp_page_bytes: NULL argument");
+    *bytes = (size_t)2 * kvp::kPage * ctx->d.g * ctx->d.d_h * ctx->esize();
+    return ok();
+}
+
 namespace {
 
 // ---- training --------------------------------------------------------------
@@ -640,12 +690,14 @@ int check_prefill_args(const kvp_ctx* ctx, const void* x, const void* y, int B, 
 
 }  // namespace
 
-extern "C" int kvp_prefill(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* ws,
-                           size_t ws_bytes, void* stream) {
+namespace {
+
+int prefill_impl(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* ws, size_t ws_bytes,
+                 void* stream, const PageTable* pt) {
     Workspace w;
     int rc = check_prefill_args(ctx, x, y, B, S, ws, ws_bytes, &w);
     if (rc) return rc;
-    if ((rc = check_layers(ctx, 0, ctx->d.L))) return rc;
+    if ((rc = check_layers(ctx, 0, ctx->d.L, pt != nullptr))) return rc;
     hipStream_t st = (hipStream_t)stream;
     char* base = (char*)ws;
     if (ctx->bf16() && (rc = timed(ctx, KVP_K_ROPE_TABLE, st, [&] {
@@ -657,9 +709,37 @@ extern "C" int kvp_prefill(kvp_ctx* ctx, const void* x, void* y, int B, int S, v
     const int L = ctx->d.L;
     for (int l = 0; l < L; ++l) {
         const LayerIO io = stack_io(ctx->bf16(), l, L, x, y, base, w);
-        if ((rc = run_prefill_layer(ctx, l, io, base + w.o, base, w, B, S, st))) return rc;
+        if ((rc = run_prefill_layer(ctx, l, io, base + w.o, base, w, B, S, st, nullptr, nullptr, pt))) return rc;
     }
     return ok();
+}
+
+// Host checks shared by the paged entry points.
+int check_paged(const kvp_ctx* ctx, const int32_t* pages, int stride, const char* who) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "%s: NULL ctx", who);
+    if (!ctx->bf16()) return fail(KVP_E_SHAPE, "%s: paged KV storage needs a bf16 model", who);
+    if (!pages || stride < 1) return fail(KVP_E_INVALID_ARG, "%s: NULL page table or stride < 1", who);
+    if ((int64_t)stride * kvp::kPage > INT32_MAX / 2)
+        return fail(KVP_E_INVALID_ARG, "%s: page table stride %d too large", who, stride);
+    return KVP_OK;
+}
+
+}  // namespace
+
+extern "C" int kvp_prefill(kvp_ctx* ctx, const void* x, void* y, int B, int S, void* ws,
+                           size_t ws_bytes, void* stream) {
+    return prefill_impl(ctx, x, y, B, S, ws, ws_bytes, stream, nullptr);
+}
+
+extern "C" int kvp_prefill_paged(kvp_ctx* ctx, const void* x, void* y, int B, int S, const int32_t* pages,
+                                 int pages_stride, void* ws, size_t ws_bytes, void* stream) {
+    int rc;
+    if ((rc = check_paged(ctx, pages, pages_stride, "kvp_prefill_paged"))) return rc;
+    if (S > kvp::kPage * pages_stride)
+        return fail(KVP_E_CAPACITY, "kvp_prefill_paged: S=%d exceeds the page table's reach (%d positions)", S,
+                    kvp::kPage * pages_stride);
+    const PageTable pt{pages, pages_stride};
+    return prefill_impl(ctx, x, y, B, S, ws, ws_bytes, stream, &pt);
 }
 
 extern "C" int kvp_layer_forward(kvp_ctx* ctx, int l, const void* x, void* attn_out, void* y, int B,
@@ -683,16 +763,19 @@ extern "C" int kvp_layer_forward(kvp_ctx* ctx, int l, const void* x, void* attn_
     return run_prefill_layer(ctx, l, io, attn_out ? attn_out : base + w.o, base, w, B, S, st);
 }
 
-extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
-                               void* y, int B, void* ws, size_t ws_bytes, void* stream) {
+namespace {
+
+int decode_impl(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len, void* y, int B, void* ws,
+                size_t ws_bytes, void* stream, const PageTable* pt) {
     if (!ctx || !x || !y || !len_dev) return fail(KVP_E_INVALID_ARG, "decode: NULL argument");
     if (x == y) return fail(KVP_E_INVALID_ARG, "decode: x and y must not alias");
     if (!aligned16(x) || !aligned16(y)) return fail(KVP_E_INVALID_ARG, "decode: x, y must be 16-byte aligned");
     if (B < 1 || max_len < 0) return fail(KVP_E_INVALID_ARG, "decode: B >= 1 and max_len >= 0 required");
     if (B > ctx->d.max_batch) return fail(KVP_E_CAPACITY, "decode: B=%d > max_batch=%d", B, ctx->d.max_batch);
-    if (max_len >= ctx->d.kv_capacity)
-        return fail(KVP_E_CAPACITY, "decode: position %d does not fit kv_capacity=%d", max_len,
-                    ctx->d.kv_capacity);
+    const int reach = pt ? kvp::kPage * pt->stride : ctx->d.kv_capacity;
+    if (max_len >= reach)
+        return fail(KVP_E_CAPACITY, "decode: position %d does not fit %s=%d", max_len,
+                    pt ? "the page table's reach" : "kv_capacity", reach);
     if (ctx->bf16() && B > kDecodeMaxRows)
         return fail(KVP_E_SHAPE, "decode: bf16 decode handles at most %d sequences per call", kDecodeMaxRows);
     const Workspace w = layout(*ctx, KVP_PHASE_DECODE, B, 1);
@@ -700,15 +783,31 @@ extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_d
         return fail(KVP_E_WORKSPACE, "decode: workspace needs %zu bytes (16-byte aligned), got %zu",
                     w.total, ws ? ws_bytes : (size_t)0);
     int rc;
-    if ((rc = check_layers(ctx, 0, ctx->d.L))) return rc;
+    if ((rc = check_layers(ctx, 0, ctx->d.L, pt != nullptr))) return rc;
     hipStream_t st = (hipStream_t)stream;
     char* base = (char*)ws;
     const int L = ctx->d.L;
     for (int l = 0; l < L; ++l) {
         const LayerIO io = stack_io(ctx->bf16(), l, L, x, y, base, w);
-        if ((rc = run_decode_layer(ctx, l, io, len_dev, max_len, base, w, B, st))) return rc;
+        if ((rc = run_decode_layer(ctx, l, io, len_dev, max_len, base, w, B, st, pt))) return rc;
     }
     return ok();
+}
+
+}  // namespace
+
+extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
+                               void* y, int B, void* ws, size_t ws_bytes, void* stream) {
+    return decode_impl(ctx, x, len_dev, max_len, y, B, ws, ws_bytes, stream, nullptr);
+}
+
+extern "C" int kvp_decode_step_paged(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
+                                     const int32_t* pages, int pages_stride, void* y, int B, void* ws,
+                                     size_t ws_bytes, void* stream) {
+    int rc;
+    if ((rc = check_paged(ctx, pages, pages_stride, "kvp_decode_step_paged"))) return rc;
+    const PageTable pt{pages, pages_stride};
+    return decode_impl(ctx, x, len_dev, max_len, y, B, ws, ws_bytes, stream, &pt);
 }
 
 // ============================================================================

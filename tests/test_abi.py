@@ -6,6 +6,7 @@ import os
 import random
 import re
 
+import numpy as np
 import pytest
 
 from oracle import planner as opl
@@ -322,3 +323,94 @@ def test_calibration_entry_points_reject_bad_arguments():
     assert L.kvp_calib_stream_read(C.c_void_p(256), 1000, C.c_void_p(16), None) == kb.KVP_E_INVALID_ARG
     assert L.kvp_calib_stream_read(C.c_void_p(258), 65536, C.c_void_p(16), None) == kb.KVP_E_INVALID_ARG
     assert "kvp_calib_stream_read" in L.kvp_last_error().decode()
+
+
+def test_pager_allocates_all_or_nothing_and_reuses_pages():
+    """kvp_pager_*: lowest pages first from a fresh pager, all-or-nothing growth, release."""
+    p = kb.Pager(10, 3, 4)
+    assert p.free_pages() == 10
+    p.reserve(0, 130)                       # 3 pages: 0, 1, 2
+    assert p.rows([0]).tolist() == [[0, 1, 2, -1]]
+    p.reserve(0, 128)                       # never shrinks
+    assert p.rows([0]).tolist() == [[0, 1, 2, -1]]
+    p.reserve(1, 64)                        # exactly one page
+    assert p.rows([1])[0, 0] == 3
+    assert not p.try_reserve(2, 5 * 64)     # beyond the row (4 pages): nothing reserved
+    assert p.free_pages() == 6
+    p.reserve(2, 4 * 64)
+    assert p.free_pages() == 2
+    assert not p.try_reserve(1, 4 * 64)     # 3 more pages needed, 2 free: nothing changes
+    assert p.rows([1]).tolist() == [[3, -1, -1, -1]] and p.free_pages() == 2
+    p.release(0)
+    assert p.free_pages() == 5 and p.rows([0]).tolist() == [[-1] * 4]
+    p.reserve(1, 4 * 64)                    # the released pages come back first, in order
+    assert p.rows([1]).tolist() == [[3, 0, 1, 2]]
+    with pytest.raises(kb.KvpError) as e:
+        p.reserve(3, 1)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    p.close()
+
+
+def test_pager_random_operations_keep_pages_disjoint():
+    rng = np.random.RandomState(3)
+    n_pages, seqs, row = 200, 12, 40
+    p = kb.Pager(n_pages, seqs, row)
+    held = [0] * seqs
+    for _ in range(2000):
+        s = int(rng.randint(seqs))
+        if rng.rand() < 0.2:
+            p.release(s)
+            held[s] = 0
+            continue
+        n = int(rng.randint(0, row * 64 + 200))
+        need = (n + 63) // 64
+        free_before = p.free_pages()
+        okay = p.try_reserve(s, n)
+        add = max(0, need - held[s])
+        assert okay == (need <= row and add <= free_before)
+        if okay:
+            held[s] = max(held[s], need)
+        tab = p.rows(list(range(seqs)))
+        mapped = tab[tab >= 0]
+        assert len(mapped) == sum(held) == n_pages - p.free_pages()
+        assert len(np.unique(mapped)) == len(mapped)          # no page in two places
+        assert mapped.max(initial=-1) < n_pages
+        for t in range(seqs):                                   # rows are prefixes
+            assert (tab[t, :held[t]] >= 0).all() and (tab[t, held[t]:] == -1).all()
+    p.close()
+
+
+def test_paged_entry_points_host_checks():
+    m = kb.Model(2, 256, 2, 1, 128, kb.KVP_DTYPE_BF16, [0, 0], max_batch=2, max_seq=200,
+                 kv_capacity=256)
+    assert m.kvp_page_bytes() == 2 * 64 * 1 * 128 * 2
+    fake = 1 << 20
+    with pytest.raises(kb.KvpError) as e:            # consumer owns no pool
+        m.kvp_set_kv_pool(1, fake, fake, 4)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    with pytest.raises(kb.KvpError) as e:
+        m.kvp_set_kv_pool(0, fake, fake, 0)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    m.kvp_set_layer(0, fake, fake, fake, fake)
+    m.kvp_set_layer(1, fake, 0, 0, fake)
+    n = m.kvp_workspace_size(kb.KVP_PHASE_PREFILL, 2, 200)
+    with pytest.raises(kb.KvpError) as e:            # pools never set
+        m.kvp_prefill_paged(fake, fake * 2, 2, 200, fake * 3, 4, fake * 4, n)
+    assert e.value.code == kb.KVP_E_STATE
+    m.kvp_set_kv_pool(0, fake, fake, 8)
+    with pytest.raises(kb.KvpError) as e:            # S beyond the table's reach
+        m.kvp_prefill_paged(fake, fake * 2, 2, 200, fake * 3, 3, fake * 4, n)
+    assert e.value.code == kb.KVP_E_CAPACITY
+    with pytest.raises(kb.KvpError) as e:            # no table
+        m.kvp_prefill_paged(fake, fake * 2, 2, 200, 0, 4, fake * 4, n)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    nd = m.kvp_workspace_size(kb.KVP_PHASE_DECODE, 2)
+    with pytest.raises(kb.KvpError) as e:            # position 256 beyond a 4-page row
+        m.kvp_decode_step_paged(fake, fake * 8, 256, fake * 3, 4, fake * 2, 2, fake * 4, nd)
+    assert e.value.code == kb.KVP_E_CAPACITY
+    m.close()
+    f = kb.Model(1, 64, 1, 1, 64, kb.KVP_DTYPE_FP32, [0], max_batch=1, max_seq=8, kv_capacity=8)
+    with pytest.raises(kb.KvpError) as e:
+        f.kvp_set_kv_pool(0, fake, fake, 4)
+    assert e.value.code == kb.KVP_E_SHAPE
+    f.close()
