@@ -107,7 +107,7 @@ class Stack:
     not fit in HBM; timing is unaffected because every slot is far larger than the caches)."""
 
     def __init__(self, w: ki.Workload, B: int, max_seq: int, cap: int, fill_npos: int = 0,
-                 alias_of=None):
+                 alias_of=None, slots: bool = True):
         import torch
         from kvp_inputs import device as kd
         from paper_2608_15943_amd import binding as kb
@@ -128,7 +128,7 @@ class Stack:
                 kd.fill_weight(w, kind, l, t[name].data_ptr())
             self.model.kvp_set_layer(l, t["wq"].data_ptr(), t["wk"].data_ptr() if prod else 0,
                                      t["wv"].data_ptr() if prod else 0, t["wo"].data_ptr())
-            if prod:
+            if prod and slots:
                 if alias_of and l in alias_of:
                     K, V = self.keep[alias_of[l]]["K"], self.keep[alias_of[l]]["V"]
                 else:
@@ -495,7 +495,7 @@ def main():
                     help="skip the achievable-peak calibration (no frac_achievable figures)")
     ap.add_argument("--no-train", action="store_true", help="skip the training-step line")
     ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib",
-                                       "train"],
+                                       "train", "decode_capacity"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
@@ -529,6 +529,8 @@ def main():
             out = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
         elif args.only == "train":
             out = train_entry(ki.stage_share_prefill(), steps_d, warm_d)
+        elif args.only == "decode_capacity":
+            out = capacity_entry(steps_d, warm_d)
         else:
             w = ki.stage_share_prefill()
             ms, prof, finite = bench_prefill(w, args.steps, args.warmup)
@@ -604,6 +606,7 @@ def main():
                 "kv_cache_bytes_shared": kv_bytes(wd), "kv_cache_bytes_unshared": kv_bytes(wi)}
         if not args.no_extra:
             result["decode_ragged_128k"] = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
+            result["decode_capacity"] = capacity_entry(steps_d, warm_d)
 
     if not args.no_cpu:
         log(f"[bench] oracle CPU baseline ({args.cpu_seq} positions of one sequence)")
@@ -640,6 +643,118 @@ def decode_entry(wd: ki.Workload, steps: int, warmup: int, alias_of=None):
     }
     log(f"[bench] decode {dms:.3f} ms/step, {out['tokens_per_s']} tok/s, "
         f"attention {rl['achieved']:.0f} GB/s")
+    return out
+
+
+PAGE = 64
+
+
+def paged_decode(w: ki.Workload, lens, table, n_pages: int, steps: int, warmup: int):
+    """One decode step over len(lens) sequences whose caches live in n_pages-page pools under
+    `table` (host int32 [B][row]), timed like bench_decode."""
+    import torch
+    from kvp_inputs import device as kd
+    from paper_2608_15943_amd import binding as kb
+    B, row = len(lens), table.shape[1]
+    t0 = time.perf_counter()
+    st = Stack(w, B, 1, PAGE, slots=False)
+    pools = []
+    tab_t = torch.from_numpy(np.ascontiguousarray(table)).cuda()
+    lens_t = torch.tensor(lens, dtype=torch.int32, device="cuda")
+    for l in w.producers():
+        K = torch.empty((w.g, n_pages, PAGE, w.d_h), dtype=torch.bfloat16, device="cuda")
+        V = torch.empty((w.g, n_pages, w.d_h, PAGE), dtype=torch.bfloat16, device="cuda")
+        kd.fill_cache_pages(w, l, K.data_ptr(), V.data_ptr(), tab_t.data_ptr(), row, n_pages, lens_t.data_ptr(), B)
+        st.model.kvp_set_kv_pool(l, K.data_ptr(), V.data_ptr(), n_pages)
+        pools.append((K, V))
+    torch.cuda.synchronize()
+    log(f"[bench] paged decode {w.name} B={B} setup {time.perf_counter() - t0:.1f}s "
+        f"({torch.cuda.memory_allocated() / 2**30:.1f} GiB resident)")
+    x = torch.empty((B, w.h), dtype=torch.bfloat16, device="cuda")
+    kd.fill_decode_x(w, x.data_ptr(), B)
+    y = torch.empty_like(x)
+    max_len = int(np.max(lens))
+    n = st.model.kvp_workspace_size(kb.KVP_PHASE_DECODE, B)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    cs = torch.cuda.current_stream().cuda_stream
+
+    def run():
+        st.model.kvp_decode_step_paged(x.data_ptr(), lens_t.data_ptr(), max_len, tab_t.data_ptr(), row,
+                                       y.data_ptr(), B, ws.data_ptr(), n, cs)
+
+    ms, prof = time_steps(run, st.model, steps, warmup)
+    fin = bool(torch.isfinite(y.float()).all().item())
+    del st, pools, x, y, ws, tab_t, lens_t
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+    return ms, prof, fin
+
+
+def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0, max_rows: int = 64):
+    """Capacity-driven decode (paged KV storage): with budget_gib of HBM for the KV cache, how
+    many sequences of the ragged 64K-128K stream fit (admitted in order until the pool is
+    full), for the shared map and the identity map, in 64-position pages and in contiguous
+    slots at the 128K capacity; then one decode step over every admitted sequence, timed for
+    both maps on pages.  Also the cost of paging itself: the 8-sequence ragged workload on
+    pages against the same workload on slots."""
+    import dataclasses
+
+    from paper_2608_15943_amd import binding as kb
+    base = ki.decode_128k_ragged()
+    stream = dataclasses.replace(base, batch=max_rows).lengths()
+    row = base.kv_capacity // PAGE
+    budget = int(budget_gib * 2**30)
+    out = {"workload": base.name + "-capacity", "kv_budget_bytes": budget, "page_positions": PAGE,
+           "context_distribution": [base.ctx_lo, base.ctx_hi], "maps": {}}
+    for label, w in (("shared", base), ("identity", base.with_map(list(range(base.L)), "-identity"))):
+        nprod = len(w.producers())
+        page_bytes = 2 * PAGE * w.g * w.d_h * 2
+        n_pages = budget // (page_bytes * nprod)
+        slot_seqs = budget // (nprod * 2 * w.g * w.kv_capacity * w.d_h * 2)
+        pager = kb.Pager(n_pages, max_rows, row)
+        B = 0
+        while B < max_rows and pager.try_reserve(B, int(stream[B]) + 1):
+            B += 1
+        lens = stream[:B]
+        tab = pager.rows(list(range(B)))
+        used = n_pages - pager.free_pages()
+        pager.close()
+        log(f"[bench] capacity {label}: {B} sequences on {used}/{n_pages} pages per producer "
+            f"(contiguous 128K slots: {slot_seqs})")
+        ms, prof, fin = paged_decode(w, lens, tab, n_pages, steps, warmup)
+        db = decode_bytes(w, lens)
+        ctx = int(np.sum(lens.astype(np.int64) + 1))
+        n_a = prof["dec_attn"][0]
+        rl = roofline_entry("dec_attn", prof, 2 * w.g * w.d_h * 2, ctx * w.L * steps / n_a,
+                            PEAK_HBM_GBS, "GB/s", "hbm", w.name + "-paged")
+        rl["per_unit"] = "bytes of K and V read for one cached position of one layer (g*d_h*2*2)"
+        out["maps"][label] = {
+            "producers": nprod, "pages_per_producer": int(n_pages), "pages_used": int(used),
+            "max_sequences_paged": B, "max_sequences_contiguous_128k": int(slot_seqs),
+            "resident_tokens": ctx, "context": [int(lens.min()), int(lens.max())],
+            "ms_per_step": round(ms, 4), "tokens_per_s": round(B / (ms * 1e-3), 2),
+            "hbm_gbs": round(sum(db.values()) / (ms * 1e-3) / 1e9, 1), "finite": fin, "roofline": rl,
+            "kernels": {k: {"launches": c, "avg_ms": round(t / c, 5)} for k, (c, t) in prof.items()}}
+        log(f"[bench] capacity {label}: {ms:.2f} ms/step, {B / (ms * 1e-3):.1f} tok/s, "
+            f"attention {rl['achieved']:.0f} GB/s")
+    sh, idn = out["maps"]["shared"], out["maps"]["identity"]
+    out["shared_vs_identity"] = {
+        "sequences_paged": round(sh["max_sequences_paged"] / max(idn["max_sequences_paged"], 1), 3),
+        "sequences_contiguous": round(sh["max_sequences_contiguous_128k"] /
+                                      max(idn["max_sequences_contiguous_128k"], 1), 3),
+        "tokens_per_s": round(sh["tokens_per_s"] / idn["tokens_per_s"], 4)}
+    # Paging overhead: the 8-sequence ragged workload, pages vs slots.
+    lens8 = base.lengths()
+    pager = kb.Pager(int(np.sum((lens8.astype(np.int64) + PAGE) // PAGE)), base.batch, row)
+    for b, L in enumerate(lens8):
+        pager.reserve(b, int(L) + 1)
+    tab8 = pager.rows(list(range(base.batch)))
+    pager.close()
+    ms_p, _, _ = paged_decode(base, lens8, tab8, int(tab8.max()) + 1, steps, warmup)
+    ms_s, _, _, _ = bench_decode(base, steps, warmup)
+    out["paged_vs_slots_b8"] = {"paged_ms_per_step": round(ms_p, 4), "slots_ms_per_step": round(ms_s, 4),
+                                "ratio": round(ms_p / ms_s, 4)}
+    log(f"[bench] 8-sequence ragged decode: pages {ms_p:.3f} ms, slots {ms_s:.3f} ms")
     return out
 
 

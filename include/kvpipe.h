@@ -333,8 +333,9 @@ int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max
  * as the pools have pages, whatever the mix of lengths, and a consumer layer adds
  * no pages.
  *
- * Page layout (bf16 models): producer l's pool K [n_pages][g][64][d_h] and
- * V [n_pages][g][d_h][64] (V transposed within the page, as in the slots).  A
+ * Page layout (bf16 models): producer l's head-major pools K [g][n_pages][64][d_h]
+ * and V [g][n_pages][d_h][64] (V transposed within the page, as in the slots), so
+ * a run of consecutive pages is one contiguous stream per KV head, as a slot is.  A
  * device page table pages [B][stride] (int32, row b for sequence b of the call)
  * maps position p of sequence b to page pages[b][p / 64], row p % 64, in every
  * producer's pool.  Entries are clamped to [0, n_pages) on the device, so a bad

@@ -31,8 +31,8 @@ def _lib():
                                  C.c_void_p]
         L.kvpin_fill.restype = C.c_int
         L.kvpin_fill_pages.argtypes = [C.c_void_p, C.c_int, C.c_uint64, C.c_float, C.c_void_p, C.c_int,
-                                       C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int, C.c_uint64,
-                                       C.c_uint64, C.c_void_p]
+                                       C.c_int, C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int,
+                                       C.c_uint64, C.c_uint64, C.c_void_p]
         L.kvpin_fill_pages.restype = C.c_int
         _LIB = L
     return _LIB
@@ -87,8 +87,8 @@ def fill_cache(w: Workload, layer: int, k_ptr: int, v_ptr: int, B: int, cap: int
 
 
 def fill_cache_pages(w: Workload, layer: int, k_pool: int, v_pool: int, pages_dev: int, stride: int,
-                     npos_dev: int, B: int, stream: int = 0) -> None:
-    """Producer ``layer``'s page pools (K [n][g][64][d], V [n][g][d][64]) hold the same
+                     n_pages: int, npos_dev: int, B: int, stream: int = 0) -> None:
+    """Producer ``layer``'s page pools (K [g][n][64][d], V [g][n][d][64]) hold the same
     values as fill_cache's slots: position p < npos[b] of sequence b at page
     pages[b][p // 64], row p % 64 (device int32 arrays pages [B][stride], npos [B])."""
     g, d = w.g, w.d_h
@@ -96,7 +96,7 @@ def fill_cache_pages(w: Workload, layer: int, k_pool: int, v_pool: int, pages_de
     sc = C.c_float(float(normal_scale(w.cache_sigma)))
     for tid, ptr, tr in ((tensor_id(KIND_KCACHE, layer), k_pool, 0), (tensor_id(KIND_VCACHE, layer), v_pool, 1)):
         rc = _lib().kvpin_fill_pages(C.c_void_p(ptr), kind, C.c_uint64(stream_key(w.seed, tid)), sc,
-                                     C.c_void_p(pages_dev), stride, C.c_void_p(npos_dev), B, g, d, tr,
+                                     C.c_void_p(pages_dev), stride, n_pages, C.c_void_p(npos_dev), B, g, d, tr,
                                      C.c_uint64(g * POS_STRIDE * d), C.c_uint64(POS_STRIDE * d),
                                      C.c_void_p(stream or None))
         if rc != 0:

@@ -49,11 +49,12 @@ __global__ void fill_kernel(void* dst, int kind, uint64_t key, float scale, int6
 
 // Paged cache: element (b, h, pos, c) of the logical cache [B][g][POS][d] (logical index
 // b * lb + h * lh + pos * d + c) for pos < npos[b], stored at page pt[b * stride + pos / 64],
-// row pos % 64 of a pool [n][g][64][d] (transposed = 0) or [n][g][d][64] (transposed = 1).
+// row pos % 64 of a head-major pool [g][n][64][d] (transposed = 0) or [g][n][d][64]
+// (transposed = 1).
 // Unmapped (negative) entries are skipped.
 __global__ void fill_pages_kernel(void* dst, int kind, uint64_t key, float scale, const int32_t* pt,
-                                  int stride, const int32_t* npos, int g, int d, int transposed,
-                                  uint64_t lb, uint64_t lh, int64_t total) {
+                                  int stride, int n_pages, const int32_t* npos, int g, int d,
+                                  int transposed, uint64_t lb, uint64_t lh, int64_t total) {
     for (int64_t t = blockIdx.x * (int64_t)blockDim.x + threadIdx.x; t < total;
          t += (int64_t)gridDim.x * blockDim.x) {
         int64_t r = t;
@@ -76,9 +77,9 @@ __global__ void fill_pages_kernel(void* dst, int kind, uint64_t key, float scale
         const int pos = 64 * j + row;
         if (pos >= npos[b]) continue;
         const int pg = pt[(int64_t)b * stride + j];
-        if (pg < 0) continue;
-        const int64_t off = transposed ? (((int64_t)pg * g + h) * d + c) * 64 + row
-                                       : (((int64_t)pg * g + h) * 64 + row) * d + c;
+        if (pg < 0 || pg >= n_pages) continue;
+        const int64_t off = transposed ? (((int64_t)h * n_pages + pg) * d + c) * 64 + row
+                                       : (((int64_t)h * n_pages + pg) * 64 + row) * d + c;
         const uint64_t idx = (uint64_t)b * lb + (uint64_t)h * lh + (uint64_t)pos * d + (uint64_t)c;
         const float v = normal_at(key, idx, scale);
         if (kind == 0)
@@ -91,14 +92,15 @@ __global__ void fill_pages_kernel(void* dst, int kind, uint64_t key, float scale
 }  // namespace
 
 extern "C" int kvpin_fill_pages(void* dst, int kind, uint64_t key, float scale, const int32_t* pt, int stride,
-                                const int32_t* npos, int B, int g, int d, int transposed, uint64_t lb,
-                                uint64_t lh, void* stream) {
-    if (!dst || !pt || !npos || B < 1 || g < 1 || d < 1 || stride < 1 || (kind != 0 && kind != 1)) return -1;
+                                int n_pages, const int32_t* npos, int B, int g, int d, int transposed,
+                                uint64_t lb, uint64_t lh, void* stream) {
+    if (!dst || !pt || !npos || B < 1 || g < 1 || d < 1 || stride < 1 || n_pages < 1 || (kind != 0 && kind != 1))
+        return -1;
     const int64_t total = (int64_t)B * stride * g * 64 * d;
     int64_t blocks = (total + 255) / 256;
     if (blocks > 65536) blocks = 65536;
     hipLaunchKernelGGL(fill_pages_kernel, dim3((unsigned)blocks), dim3(256), 0, (hipStream_t)stream, dst, kind,
-                       key, scale, pt, stride, npos, g, d, transposed, lb, lh, total);
+                       key, scale, pt, stride, n_pages, npos, g, d, transposed, lb, lh, total);
     return hipGetLastError() == hipSuccess ? 0 : -2;
 }
 

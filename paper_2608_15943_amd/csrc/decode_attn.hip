@@ -97,15 +97,25 @@ __global__ __launch_bounds__(64, 1) void decode_attn_kernel(
     // Position held by MFMA row rho (= lane & 15 for the A operand) of score block tb
     // of a tile: block 2s + e covers positions 32 s + 8 (rho / 4) + 4 e + rho % 4.
     // Tiles start at multiples of 64 and cap % 64 == 0, so every load stays in the slot
-    // (or, paged, in the tile's page).
+    // (or, paged, in the tile's page).  Paged: the wave keeps 64 consecutive entries of a
+    // table row in a register (lane i: entry 64 c + i of row pb) and reads the tile's entry
+    // with readlane, so a dependent table load is paid once per 64 tiles, not per tile.
+    int pb = -1, pc = -1, pgv = 0;
     auto load = [&](int lb, int lh, int t0, DTile& tl) {
         const uint16_t* kbase;
         const uint16_t* vbase;
         int vld;
         if constexpr (PAGED) {
-            const int pg = page_at(pages, lb, t0 / TILE);
-            kbase = Kc + ((size_t)pg * g + lh) * TILE * D - (size_t)t0 * D;
-            vbase = Vc + ((size_t)pg * g + lh) * D * TILE - t0;
+            const int j = t0 / TILE;
+            if (lb != pb || (j >> 6) != pc) {
+                pb = lb;
+                pc = j >> 6;
+                const int e = 64 * pc + lane;
+                pgv = e < pages.stride ? pages.pt[(size_t)lb * pages.stride + e] : 0;
+            }
+            const int pg = min(max(__builtin_amdgcn_readlane(pgv, j & 63), 0), pages.n - 1);
+            kbase = Kc + ((size_t)lh * pages.n + pg) * TILE * D - (size_t)t0 * D;
+            vbase = Vc + ((size_t)lh * pages.n + pg) * D * TILE - t0;
             vld = TILE;
         } else {
             kbase = Kc + ((size_t)lb * g + lh) * cap * D;

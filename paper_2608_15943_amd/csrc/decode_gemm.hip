@@ -175,15 +175,18 @@ __global__ __launch_bounds__(256) void decode_qkv_epi_kernel(const float* __rest
     __shared__ float2 cs[HALF];
     const int b = blockIdx.y;
     const int pos = max(0, min(lens[b], cap - 1));   // never outside the slot (or page table row)
-    // Slot (b, kv head 0) base and the row of pos, in units of D elements.
-    size_t kv0;
+    // Rows (in units of D elements) of head 0's block holding pos and the stride between
+    // heads' blocks: the slot of sequence b, or page pos / 64 of the head-major pools.
+    size_t kv0, hstride;
     int vld, row;
     if (pages.pt) {
-        kv0 = (size_t)page_at(pages, b, pos / kPage) * g * kPage;
+        kv0 = (size_t)page_at(pages, b, pos / kPage) * kPage;
+        hstride = (size_t)pages.n * kPage;
         vld = kPage;
         row = pos % kPage;
     } else {
         kv0 = (size_t)b * g * cap;
+        hstride = cap;
         vld = cap;
         row = pos;
     }
@@ -215,13 +218,13 @@ __global__ __launch_bounds__(256) void decode_qkv_epi_kernel(const float* __rest
             q[(size_t)b * a * D + h * D + i] = f2bf(o1);
             q[(size_t)b * a * D + h * D + i + HALF] = f2bf(o2);
         } else {
-            const size_t kb = (kv0 + (size_t)(h - a) * vld + row) * D;
+            const size_t kb = (kv0 + (size_t)(h - a) * hstride + row) * D;
             kc[kb + i] = f2bf(o1);
             kc[kb + i + HALF] = f2bf(o2);
         }
     } else {
         const int e = j - npairs, h = e / D, c = e - h * D;
-        vc[(kv0 + (size_t)h * vld) * D + (size_t)c * vld + row] = f2bf(val(a * D + g * D + e));
+        vc[(kv0 + (size_t)h * hstride) * D + (size_t)c * vld + row] = f2bf(val(a * D + g * D + e));
     }
 }
 

@@ -126,30 +126,35 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     // 16 wave + 4 j + lane / 16, four 256-byte rows per instruction.  Positions past the
     // slot (only in the last tile when cap % 128 == 64) are clamped to the slot's last
     // row / chunk: they lie beyond S, so their scores are masked and their V is zeroed.
-    // Paged, positions are clamped to the last one before S (whose page is mapped).
+    // Paged: the tile's two pages are looked up once per tile (pages past the last one
+    // holding a position < S are replaced by that page, so every read stays in a mapped
+    // page; rows of positions >= S are masked and their V zeroed as above).  Each wave keeps
+    // 64 consecutive entries of the table row in a register (lane i: entry 64 c + i) and
+    // reads the two entries with readlane: one table load per 32 tiles.  Wave w's K rows
+    // 16 w .. 16 w + 15 all lie in page w / 4 of the tile, so its K base is wave-uniform.
+    int pchunk = -1, pgv = 0;
     auto issue_tile = [&](int t, int stg) {
         const int t0 = t * BKV;
         if constexpr (PAGED) {
-            const int last = S - 1, vlast = last & ~7;
-            const int p0 = t0 / kPage;
-            const uint16_t* kp[2];
-            const uint16_t* vp[2];
-#pragma unroll
-            for (int h = 0; h < 2; ++h) {
-                const int pg = page_at(pages, b, min(p0 + h, last / kPage));
-                kp[h] = Kc + ((size_t)pg * g + kvh) * kPage * D;
-                vp[h] = Vc + ((size_t)pg * g + kvh) * D * kPage;
+            const int p0 = t0 / kPage;          // even: both pages of the tile in one chunk of 64
+            if ((p0 >> 6) != pchunk) {
+                pchunk = p0 >> 6;
+                const int e = 64 * pchunk + lane;
+                pgv = e < pages.stride ? pages.pt[(size_t)b * pages.stride + e] : 0;
             }
+            const int p1 = min(p0 + 1, (S - 1) / kPage);
+            const int pg0 = min(max(__builtin_amdgcn_readlane(pgv, p0 & 63), 0), pages.n - 1);
+            const int pg1 = min(max(__builtin_amdgcn_readlane(pgv, p1 & 63), 0), pages.n - 1);
+            const size_t hb = (size_t)kvh * pages.n;
+            const uint16_t* kw = Kc + (hb + (wave >= 4 ? pg1 : pg0)) * kPage * D;
+            const uint16_t* v0 = Vc + (hb + pg0) * D * kPage;
+            const uint16_t* v1 = Vc + (hb + pg1) * D * kPage;
 #pragma unroll
             for (int j = 0; j < 4; ++j) {
                 const int r = 16 * wave + 4 * j + (lane >> 4);
                 const int c = (lane & 15) ^ (r & 15);
-                const int pk = min(t0 + r, last);
-                load_lds_1k(kp[pk / kPage - p0] + (size_t)(pk % kPage) * D + 8 * c,
-                            &lk[stg][(16 * wave + 4 * j) * 16]);
-                const int pv = min(t0 + 8 * c, vlast);
-                load_lds_1k(vp[pv / kPage - p0] + (size_t)r * kPage + pv % kPage,
-                            &lv[stg][(16 * wave + 4 * j) * 16]);
+                load_lds_1k(kw + (size_t)(r & (kPage - 1)) * D + 8 * c, &lk[stg][(16 * wave + 4 * j) * 16]);
+                load_lds_1k((c >= 8 ? v1 : v0) + r * kPage + 8 * (c & 7), &lv[stg][(16 * wave + 4 * j) * 16]);
             }
             return;
         }

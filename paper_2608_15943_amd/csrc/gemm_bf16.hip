@@ -72,12 +72,12 @@ struct QkvEpi {
     // sequence b, KV head `head`: in the contiguous slot or in s's page.
     __device__ __forceinline__ size_t k_row(int b, int head, int s) const {
         if (o.pages.pt)
-            return (((size_t)page_at(o.pages, b, s / kPage) * o.g + head) * kPage + s % kPage) * 128;
+            return (((size_t)head * o.pages.n + page_at(o.pages, b, s / kPage)) * kPage + s % kPage) * 128;
         return (((size_t)b * o.g + head) * o.cap + s) * 128;
     }
     __device__ __forceinline__ size_t v_at(int b, int head, int n, int s) const {
         if (o.pages.pt)
-            return (((size_t)page_at(o.pages, b, s / kPage) * o.g + head) * 128 + n) * kPage + s % kPage;
+            return (((size_t)head * o.pages.n + page_at(o.pages, b, s / kPage)) * 128 + n) * kPage + s % kPage;
         return (((size_t)b * o.g + head) * 128 + n) * o.cap + s;
     }
     // Region of the wave's 128 columns: 0 = Q, 1 = K, 2 = V, -1 = past N.

@@ -16,7 +16,8 @@ struct WRows {
 
 // KV storage.  Contiguous slots (pt == nullptr): K [B][g][cap][d], V [B][g][d][cap].
 // Paged: position p of sequence b lives in page pt[b * stride + p / kPage], row p % kPage,
-// of the pools K [n][g][kPage][d] and V [n][g][d][kPage]; entries are clamped to [0, n).
+// of the head-major pools K [g][n][kPage][d] and V [g][n][d][kPage]; entries are clamped
+// to [0, n).
 constexpr int kPage = 64;
 struct Pages {
     const int32_t* pt;

@@ -48,8 +48,8 @@ def make_pools(dm, n_pages):
     pools = {}
     for l in range(w.L):
         if w.tau[l] == l:
-            K = torch.zeros((n_pages, w.g, PAGE, w.d_h), dtype=torch.bfloat16, device=DEV)
-            V = torch.zeros((n_pages, w.g, w.d_h, PAGE), dtype=torch.bfloat16, device=DEV)
+            K = torch.zeros((w.g, n_pages, PAGE, w.d_h), dtype=torch.bfloat16, device=DEV)
+            V = torch.zeros((w.g, n_pages, w.d_h, PAGE), dtype=torch.bfloat16, device=DEV)
             dm.model.kvp_set_kv_pool(l, K.data_ptr(), V.data_ptr(), n_pages)
             pools[l] = (K, V)
     return pools
@@ -62,7 +62,7 @@ def gather(pools, tab_t, b, npos):
     pg = tab_t[b].long()[idx // PAGE]
     row = idx % PAGE
     for l, (K, V) in pools.items():
-        out[l] = (K[pg, :, row, :].permute(1, 0, 2), V[pg, :, :, row].permute(1, 2, 0))
+        out[l] = (K[:, pg, row, :], V[:, pg, :, row].permute(1, 2, 0))
     return out
 
 
@@ -84,7 +84,7 @@ def test_decode_paged_equals_slots(h, a, g, tau, lens, stride):
     lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
     for l in pools:
         kd.fill_cache_pages(w, l, pools[l][0].data_ptr(), pools[l][1].data_ptr(), tab_t.data_ptr(), stride,
-                            lens_t.data_ptr(), B)
+                            n_pages, lens_t.data_ptr(), B)
     x = torch.empty((B, w.h), dtype=torch.bfloat16, device=DEV)
     kd.fill_decode_x(w, x.data_ptr(), B)
     y_c = torch.empty_like(x)
@@ -159,7 +159,7 @@ def test_decode_128k_ragged_paged_full_size():
     lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
     for l in pools:
         kd.fill_cache_pages(w, l, pools[l][0].data_ptr(), pools[l][1].data_ptr(), tab_t.data_ptr(), stride,
-                            lens_t.data_ptr(), B)
+                            n_pages, lens_t.data_ptr(), B)
     x = torch.empty((B, w.h), dtype=torch.bfloat16, device=DEV)
     kd.fill_decode_x(w, x.data_ptr(), B)
     y_c = torch.empty_like(x)
@@ -177,8 +177,8 @@ def test_decode_128k_ragged_paged_full_size():
         pg = tab_t[b].long()[idx // PAGE]
         for l, (K, V) in dm.slots.items():
             Kp, Vp = pools[l]
-            assert torch.equal(Kp[pg, :, idx % PAGE, :][0], K[b, :, L]), (b, l)
-            assert torch.equal(Vp[pg, :, :, idx % PAGE][0], V[b, :, :, L]), (b, l)
+            assert torch.equal(Kp[:, pg, idx % PAGE, :][:, 0], K[b, :, L]), (b, l)
+            assert torch.equal(Vp[:, pg, :, idx % PAGE][0], V[b, :, :, L]), (b, l)
     say("  bit-identical to the slots, appended rows included")
     del dm, pools, x, y_c, y_p, ws
     torch.cuda.synchronize()
