@@ -505,7 +505,8 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (the KV-shared block is measured on one GPU's share; "
-              f"see DESIGN.md for how it shards); --gpus {args.gpus} is not supported", file=sys.stderr)
+              f"more GPUs would each run their own stage or batch share); --gpus {args.gpus} is not supported",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch

@@ -154,7 +154,7 @@ def plan_fir(stage_of_layer: Sequence[int], P: int, f_full: Sequence[float],
     ok[0] = False
 
     z = [0] * L
-    # Line "compute baseline stage FLOPs" and the FIR of Eqs. (4)-(5).
+    # Stage FLOPs with no layer converted yet, and their FIR (Eqs. 4-5).
     F = stage_flops(stage_of_layer, P, f_full, f_share, z, f_lmhead)
     avg = f_avg(F)
     cur = max(F) / avg
