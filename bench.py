@@ -432,6 +432,50 @@ def achievable_peaks():
     return dict(ACHIEVABLE)
 
 
+def mall_probe(sizes_mib=(32, 64, 128, 192, 256, 384, 512), trials: int = 5):
+    """Does a second read of a buffer hit the 256 MB last-level (Infinity) cache?  For each
+    size: read a 2 GiB buffer (evicts), time a read of the buffer (cold), time it again at
+    once (re-read), read 64 MiB of other data, time it again; median of `trials`.  A consumer
+    layer re-reading its producer's cache from that level is only worth a schedule change if
+    the re-read is much faster than HBM."""
+    import torch
+    from paper_2608_15943_amd import binding as kb
+    st = torch.cuda.current_stream()
+    sink = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    flush = torch.empty(2 << 30, dtype=torch.uint8, device="cuda")
+    other = torch.empty(64 << 20, dtype=torch.uint8, device="cuda")
+
+    def rd(buf):
+        _check = kb.lib().kvp_calib_stream_read(buf.data_ptr(), buf.numel(), sink.data_ptr(), st.cuda_stream)
+        if _check != 0:
+            raise RuntimeError(f"kvp_calib_stream_read failed ({_check})")
+
+    def timed(buf):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(st)
+        rd(buf)
+        b.record(st)
+        b.synchronize()
+        return a.elapsed_time(b)
+
+    out = {}
+    for mib in sizes_mib:
+        buf = torch.empty(mib << 20, dtype=torch.uint8, device="cuda")
+        res = []
+        for _ in range(trials):
+            rd(flush)
+            c, w = timed(buf), timed(buf)
+            rd(other)
+            res.append((c, w, timed(buf)))
+        res.sort()
+        c, w, wi = res[len(res) // 2]
+        gb = (mib << 20) / 1e9
+        out[f"{mib}MiB"] = {"cold_gbs": round(gb / (c * 1e-3)), "reread_gbs": round(gb / (w * 1e-3)),
+                            "reread_after_64MiB_gbs": round(gb / (wi * 1e-3))}
+        del buf
+    return out
+
+
 def kernel_fracs(tflops: dict) -> dict:
     """Every MFMA kernel's algorithmic TFLOP/s against the datasheet and the measured peak."""
     ach = ACHIEVABLE.get("mfma_bf16_tflops")
@@ -495,7 +539,7 @@ def main():
                     help="skip the achievable-peak calibration (no frac_achievable figures)")
     ap.add_argument("--no-train", action="store_true", help="skip the training-step line")
     ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib",
-                                       "train", "decode_capacity"],
+                                       "train", "decode_capacity", "mall"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
@@ -517,6 +561,9 @@ def main():
     kb.lib()   # fail loudly if the HIP library is missing
     if args.only == "calib":
         print(json.dumps({"only": "calib", **achievable_peaks()}), flush=True)
+        return
+    if args.only == "mall":
+        print(json.dumps({"only": "mall", **mall_probe()}), flush=True)
         return
     if not args.no_calib and not args.only:
         log(f"[bench] achievable peaks {achievable_peaks()}")
