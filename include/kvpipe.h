@@ -314,7 +314,10 @@ int kvp_layer_forward(kvp_ctx* ctx, int l, const void* x, void* attn_out, void* 
  * Each producer appends its post-RoPE K and V at len_b before attending;
  * every layer attends over positions [0, len_b].  The caller advances the
  * lengths.  max_len (host) must be >= every len_b; it sizes the split-K
- * grid.  Sequences shorter than max_len do proportionally less work.
+ * grid.  Sequences shorter than max_len do proportionally less work.  bf16
+ * models run a batch above 64 as consecutive chunks of 64 sequences through
+ * the whole stack (each chunk reads the weights once); results do not depend
+ * on the chunking.
  * Errors: KVP_E_CAPACITY if max_len >= kv_capacity or B > max_batch (len_b
  * itself is not read on the host; len_b > max_len is undefined behaviour),
  * KVP_E_INVALID_ARG, KVP_E_WORKSPACE, KVP_E_STATE, KVP_E_HIP.

@@ -216,8 +216,14 @@ struct KvView {
     kvp::Pages pages;
 };
 
-KvView kv_view(const kvp_ctx* c, const Layer& P, const PageTable* pt) {
-    if (!pt) return {P.kc, P.vc, c->d.kv_capacity, kvp::Pages{nullptr, 0, 0}};
+// seq0: index of the call's first sequence in the slots (decode runs large batches in
+// chunks; a chunk's page table rows are passed already offset).
+KvView kv_view(const kvp_ctx* c, const Layer& P, const PageTable* pt, int seq0 = 0) {
+    if (!pt) {
+        const size_t off = (size_t)seq0 * c->d.g * c->d.kv_capacity * c->d.d_h * c->esize();
+        return {P.kc ? (char*)P.kc + off : nullptr, P.vc ? (char*)P.vc + off : nullptr, c->d.kv_capacity,
+                kvp::Pages{nullptr, 0, 0}};
+    }
     return {P.kp, P.vp, kvp::kPage * pt->stride, kvp::Pages{pt->pt, pt->stride, P.n_pages}};
 }
 
@@ -314,11 +320,11 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
 
 int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
                      int max_len, char* ws, const Workspace& w, int B, hipStream_t st,
-                     const PageTable* pt = nullptr) {
+                     const PageTable* pt = nullptr, int seq0 = 0) {
     const int p = c->tau[l];
     const bool producer = p == l;
     const Layer& P = c->layers[p];
-    const KvView kv = kv_view(c, P, pt);
+    const KvView kv = kv_view(c, P, pt, seq0);
     const int h = c->d.h, nq = c->n_q();
     const int N = producer ? nq + 2 * c->n_kv() : nq;
     const kvp::WRows wr = proj_rows(c, l, producer);
@@ -776,20 +782,33 @@ int decode_impl(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len
     if (max_len >= reach)
         return fail(KVP_E_CAPACITY, "decode: position %d does not fit %s=%d", max_len,
                     pt ? "the page table's reach" : "kv_capacity", reach);
-    if (ctx->bf16() && B > kDecodeMaxRows)
-        return fail(KVP_E_SHAPE, "decode: bf16 decode handles at most %d sequences per call", kDecodeMaxRows);
-    const Workspace w = layout(*ctx, KVP_PHASE_DECODE, B, 1);
-    if (!ws || ws_bytes < w.total || !aligned16(ws))
+    const Workspace wfull = layout(*ctx, KVP_PHASE_DECODE, B, 1);
+    if (!ws || ws_bytes < wfull.total || !aligned16(ws))
         return fail(KVP_E_WORKSPACE, "decode: workspace needs %zu bytes (16-byte aligned), got %zu",
-                    w.total, ws ? ws_bytes : (size_t)0);
+                    wfull.total, ws ? ws_bytes : (size_t)0);
     int rc;
     if ((rc = check_layers(ctx, 0, ctx->d.L, pt != nullptr))) return rc;
     hipStream_t st = (hipStream_t)stream;
     char* base = (char*)ws;
     const int L = ctx->d.L;
-    for (int l = 0; l < L; ++l) {
-        const LayerIO io = stack_io(ctx->bf16(), l, L, x, y, base, w);
-        if ((rc = run_decode_layer(ctx, l, io, len_dev, max_len, base, w, B, st, pt))) return rc;
+    // bf16 kernels take at most kDecodeMaxRows sequences per launch; sequences are
+    // independent, so a larger batch runs as consecutive chunks through the whole stack
+    // (each chunk reads the weights once more), reusing the workspace on the same stream.
+    const int chunk = ctx->bf16() ? kDecodeMaxRows : B;
+    const size_t row_bytes = (size_t)ctx->d.h * ctx->esize();
+    for (int b0 = 0; b0 < B; b0 += chunk) {
+        const int Bc = std::min(chunk, B - b0);
+        const Workspace w = layout(*ctx, KVP_PHASE_DECODE, Bc, 1);
+        const char* xc = (const char*)x + (size_t)b0 * row_bytes;
+        char* yc = (char*)y + (size_t)b0 * row_bytes;
+        PageTable ptc{};
+        if (pt) ptc = PageTable{pt->pt + (size_t)b0 * pt->stride, pt->stride};
+        for (int l = 0; l < L; ++l) {
+            const LayerIO io = stack_io(ctx->bf16(), l, L, xc, yc, base, w);
+            if ((rc = run_decode_layer(ctx, l, io, len_dev + b0, max_len, base, w, Bc, st, pt ? &ptc : nullptr,
+                                       b0)))
+                return rc;
+        }
     }
     return ok();
 }

@@ -183,3 +183,65 @@ def test_decode_128k_ragged_paged_full_size():
     del dm, pools, x, y_c, y_p, ws
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def test_decode_batches_above_64_run_in_chunks():
+    """B = 130 sequences (bf16 kernels take 64 per launch): one call on slots and one on
+    scattered pages equal calls of at most 64 sequences bit for bit; sampled sequences
+    match the oracle."""
+    w = small_workload("dec-b130", 3, 512, 4, 2, [0, 0, 2], seed=33)
+    B, stride = 130, 2
+    lens = [(37 * b) % 120 for b in range(B)]
+    say(f"[decode B={B}] lens {min(lens)}..{max(lens)}")
+    npos = int(max(lens))
+    dm = build_device_model(w, B, 1, PAGE * stride, fill_cache_npos=max(npos, 1))
+    tab, n_pages = scattered_table([n + 1 for n in lens], stride, 0, seed=10)
+    pools = make_pools(dm, n_pages)
+    tab_t = torch.from_numpy(tab).to(DEV)
+    lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+    for l in pools:
+        kd.fill_cache_pages(w, l, pools[l][0].data_ptr(), pools[l][1].data_ptr(), tab_t.data_ptr(), stride,
+                            n_pages, lens_t.data_ptr(), B)
+    x = torch.empty((B, w.h), dtype=torch.bfloat16, device=DEV)
+    kd.fill_decode_x(w, x.data_ptr(), B)
+    ws, n = workspace(dm, kb.KVP_PHASE_DECODE, B)
+    st = torch.cuda.current_stream().cuda_stream
+    slots0 = {l: (K.clone(), V.clone()) for l, (K, V) in dm.slots.items()}
+    y_all = torch.full_like(x, float("nan"))
+    dm.model.kvp_decode_step(x.data_ptr(), lens_t.data_ptr(), npos, y_all.data_ptr(), B, ws.data_ptr(), n, st)
+    yp_all = torch.full_like(x, float("nan"))
+    dm.model.kvp_decode_step_paged(x.data_ptr(), lens_t.data_ptr(), npos, tab_t.data_ptr(), stride,
+                                   yp_all.data_ptr(), B, ws.data_ptr(), n, st)
+    torch.cuda.synchronize()
+    # Restore the slots (the call appended at len_b) and run the chunks one call each, on
+    # a model whose slots start at the chunk's first sequence.
+    y_parts = torch.full_like(x, float("nan"))
+    row = w.g * PAGE * stride * w.d_h * 2   # bytes of one sequence in a K (or V) slot, bf16
+    for b0 in range(0, B, 64):
+        Bc = min(64, B - b0)
+        mc = kb.Model(w.L, w.h, w.a, w.g, w.d_h, kb.KVP_DTYPE_BF16, w.tau, max_batch=Bc, max_seq=1,
+                      kv_capacity=PAGE * stride, rope_base=w.rope_base)
+        for l in range(w.L):
+            prod = w.tau[l] == l
+            t = dm.tensors
+            mc.kvp_set_layer(l, t[f"wq{l}"].data_ptr(), t[f"wk{l}"].data_ptr() if prod else 0,
+                             t[f"wv{l}"].data_ptr() if prod else 0, t[f"wo{l}"].data_ptr())
+            if prod:
+                K, V = slots0[l]
+                mc.kvp_set_kv_slot(l, K.data_ptr() + b0 * row, V.data_ptr() + b0 * row)
+        nc = mc.kvp_workspace_size(kb.KVP_PHASE_DECODE, Bc)
+        wsc = torch.empty(nc, dtype=torch.uint8, device=DEV)
+        mc.kvp_decode_step(x[b0:].data_ptr(), lens_t[b0:].data_ptr(), npos, y_parts[b0:].data_ptr(), Bc,
+                           wsc.data_ptr(), nc, st)
+        torch.cuda.synchronize()
+        mc.close()
+    assert torch.equal(y_all, y_parts), "chunked decode differs from separate calls"
+    assert torch.equal(y_all, yp_all), "paged chunked decode differs from the slots"
+    ows = oracle_weights(w)
+    for b in (0, 63, 64, 129):
+        L = lens[b]
+        caches = {p: (ki.cache_contents(w, ki.KIND_KCACHE, p, b, L),
+                      ki.cache_contents(w, ki.KIND_VCACHE, p, b, L)) for p in dm.slots}
+        yr = oat.decode_step(ki.decode_x(w, [b])[0], L, ows, w.tau, caches, w.a, w.g, w.d_h, w.rope_base)[0]
+        assert rel_err(to_np(y_all[b]), yr) <= 2e-2, b
+    say("  chunks bit-identical to separate calls and to pages; oracle ok")
