@@ -738,22 +738,16 @@ def paged_decode(w: ki.Workload, lens, table, n_pages: int, steps: int, warmup: 
     return ms, prof, fin
 
 
-def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0, max_rows: int = 64):
-    """Capacity-driven decode (paged KV storage): with budget_gib of HBM for the KV cache, how
-    many sequences of the ragged 64K-128K stream fit (admitted in order until the pool is
-    full), for the shared map and the identity map, in 64-position pages and in contiguous
-    slots at the 128K capacity; then one decode step over every admitted sequence, timed for
-    both maps on pages.  Also the cost of paging itself: the 8-sequence ragged workload on
-    pages against the same workload on slots."""
+def capacity_scenario(base: ki.Workload, budget: int, max_rows: int, steps: int, warmup: int):
+    """Admit the sequences of base's ragged length stream in order until a budget-sized pool
+    is full (each needs len + 1 positions), for the shared map and the identity map; then
+    time one decode step over all admitted sequences on pages."""
     import dataclasses
 
     from paper_2608_15943_amd import binding as kb
-    base = ki.decode_128k_ragged()
     stream = dataclasses.replace(base, batch=max_rows).lengths()
     row = base.kv_capacity // PAGE
-    budget = int(budget_gib * 2**30)
-    out = {"workload": base.name + "-capacity", "kv_budget_bytes": budget, "page_positions": PAGE,
-           "context_distribution": [base.ctx_lo, base.ctx_hi], "maps": {}}
+    out = {"context_distribution": [base.ctx_lo, base.ctx_hi], "maps": {}}
     for label, w in (("shared", base), ("identity", base.with_map(list(range(base.L)), "-identity"))):
         nprod = len(w.producers())
         page_bytes = 2 * PAGE * w.g * w.d_h * 2
@@ -767,9 +761,10 @@ def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0, max_rows:
         tab = pager.rows(list(range(B)))
         used = n_pages - pager.free_pages()
         pager.close()
-        log(f"[bench] capacity {label}: {B} sequences on {used}/{n_pages} pages per producer "
-            f"(contiguous 128K slots: {slot_seqs})")
-        ms, prof, fin = paged_decode(w, lens, tab, n_pages, steps, warmup)
+        log(f"[bench] capacity {w.name} {label}: {B} sequences on {used}/{n_pages} pages per producer "
+            f"(contiguous slots: {slot_seqs})")
+        wb = dataclasses.replace(w, batch=B)
+        ms, prof, fin = paged_decode(wb, lens, tab, n_pages, steps, warmup)
         db = decode_bytes(w, lens)
         ctx = int(np.sum(lens.astype(np.int64) + 1))
         n_a = prof["dec_attn"][0]
@@ -778,7 +773,7 @@ def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0, max_rows:
         rl["per_unit"] = "bytes of K and V read for one cached position of one layer (g*d_h*2*2)"
         out["maps"][label] = {
             "producers": nprod, "pages_per_producer": int(n_pages), "pages_used": int(used),
-            "max_sequences_paged": B, "max_sequences_contiguous_128k": int(slot_seqs),
+            "max_sequences_paged": B, "max_sequences_contiguous": int(slot_seqs),
             "resident_tokens": ctx, "context": [int(lens.min()), int(lens.max())],
             "ms_per_step": round(ms, 4), "tokens_per_s": round(B / (ms * 1e-3), 2),
             "hbm_gbs": round(sum(db.values()) / (ms * 1e-3) / 1e9, 1), "finite": fin, "roofline": rl,
@@ -788,11 +783,31 @@ def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0, max_rows:
     sh, idn = out["maps"]["shared"], out["maps"]["identity"]
     out["shared_vs_identity"] = {
         "sequences_paged": round(sh["max_sequences_paged"] / max(idn["max_sequences_paged"], 1), 3),
-        "sequences_contiguous": round(sh["max_sequences_contiguous_128k"] /
-                                      max(idn["max_sequences_contiguous_128k"], 1), 3),
+        "sequences_contiguous": round(sh["max_sequences_contiguous"] / max(idn["max_sequences_contiguous"], 1), 3),
         "tokens_per_s": round(sh["tokens_per_s"] / idn["tokens_per_s"], 4)}
+    return out
+
+
+def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0):
+    """Capacity-driven decode (paged KV storage): with budget_gib of HBM for the KV cache, how
+    many sequences fit, shared vs identity map, in 64-position pages and in contiguous slots
+    at the stream's capacity, and one decode step over all of them.  Two length streams of
+    the 32-layer model: ragged 64K-128K (capacity 128K) and ragged 8K-16K (capacity 16K;
+    more than 64 sequences, so decode runs in 64-sequence chunks).  Also the cost of paging
+    itself: the 8-sequence ragged workload on pages against the same workload on slots."""
+    import dataclasses
+
+    from paper_2608_15943_amd import binding as kb
+    base = ki.decode_128k_ragged()
+    budget = int(budget_gib * 2**30)
+    out = {"workload": base.name + "-capacity", "kv_budget_bytes": budget, "page_positions": PAGE}
+    out.update(capacity_scenario(base, budget, 64, steps, warmup))
+    short = dataclasses.replace(base, name="decode-32L-d4096-gqa32x8-ctx8k-16k", ctx_lo=8192, ctx_hi=16383,
+                                kv_capacity=16384)
+    out["ctx_8k_16k"] = capacity_scenario(short, budget, 1024, steps, warmup)
     # Paging overhead: the 8-sequence ragged workload, pages vs slots.
     lens8 = base.lengths()
+    row = base.kv_capacity // PAGE
     pager = kb.Pager(int(np.sum((lens8.astype(np.int64) + PAGE) // PAGE)), base.batch, row)
     for b, L in enumerate(lens8):
         pager.reserve(b, int(L) + 1)
