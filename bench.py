@@ -539,7 +539,7 @@ def main():
                     help="skip the achievable-peak calibration (no frac_achievable figures)")
     ap.add_argument("--no-train", action="store_true", help="skip the training-step line")
     ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib",
-                                       "train", "decode_capacity", "mall"],
+                                       "train", "decode_capacity", "mall", "decode_graph"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
@@ -579,6 +579,8 @@ def main():
             out = train_entry(ki.stage_share_prefill(), steps_d, warm_d)
         elif args.only == "decode_capacity":
             out = capacity_entry(steps_d, warm_d)
+        elif args.only == "decode_graph":
+            out = graph_entry(args.steps, args.warmup)
         else:
             w = ki.stage_share_prefill()
             ms, prof, finite = bench_prefill(w, args.steps, args.warmup)
@@ -655,6 +657,7 @@ def main():
         if not args.no_extra:
             result["decode_ragged_128k"] = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
             result["decode_capacity"] = capacity_entry(steps_d, warm_d)
+            result["decode_graph"] = graph_entry(args.steps, args.warmup)
 
     if not args.no_cpu:
         log(f"[bench] oracle CPU baseline ({args.cpu_seq} positions of one sequence)")
@@ -818,6 +821,64 @@ def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0):
     out["paged_vs_slots_b8"] = {"paged_ms_per_step": round(ms_p, 4), "slots_ms_per_step": round(ms_s, 4),
                                 "ratio": round(ms_p / ms_s, 4)}
     log(f"[bench] 8-sequence ragged decode: pages {ms_p:.3f} ms, slots {ms_s:.3f} ms")
+    return out
+
+
+def graph_entry(steps: int, warmup: int, B: int = 8, ctx: int = 4096):
+    """Launch-bound decode: the 32-layer model (shared map of the 32K workload) at a small
+    batch and short context, 160 launches per step, eager against the same step captured
+    once into a HIP graph and replayed."""
+    import dataclasses
+
+    import torch
+    from kvp_inputs import device as kd
+    from paper_2608_15943_amd import binding as kb
+    w = dataclasses.replace(ki.decode_32k(), name=f"decode-32L-d4096-gqa32x8-b{B}-ctx{ctx}", batch=B, ctx=ctx,
+                            kv_capacity=ctx + PAGE)
+    st = Stack(w, B, 1, w.kv_capacity, fill_npos=ctx)
+    x = torch.empty((B, w.h), dtype=torch.bfloat16, device="cuda")
+    kd.fill_decode_x(w, x.data_ptr(), B)
+    y = torch.empty_like(x)
+    lens_t = torch.full((B,), ctx, dtype=torch.int32, device="cuda")
+    n = st.model.kvp_workspace_size(kb.KVP_PHASE_DECODE, B)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+
+    def run():
+        st.model.kvp_decode_step(x.data_ptr(), lens_t.data_ptr(), ctx, y.data_ptr(), B, ws.data_ptr(), n,
+                                 torch.cuda.current_stream().cuda_stream)
+
+    def timed(f):
+        for _ in range(warmup):
+            f()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(steps):
+            f()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) * 1e3 / steps
+
+    ms_eager = timed(run)
+    ref = y.clone()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        run()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        run()
+    torch.cuda.synchronize()
+    ms_graph = timed(g.replay)
+    same = bool(torch.equal(y, ref))
+    out = {"workload": w.name, "batch": B, "context": ctx, "launches_per_step": 5 * w.L,
+           "eager_ms_per_step": round(ms_eager, 4), "graph_ms_per_step": round(ms_graph, 4),
+           "speedup": round(ms_eager / ms_graph, 4), "tokens_per_s_graph": round(B / (ms_graph * 1e-3), 1),
+           "graph_output_equals_eager": same}
+    log(f"[bench] decode graph {w.name}: eager {ms_eager:.3f} ms, graph {ms_graph:.3f} ms")
+    del g, st, x, y, ws, lens_t
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     return out
 
 
