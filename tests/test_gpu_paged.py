@@ -245,3 +245,35 @@ def test_decode_batches_above_64_run_in_chunks():
         yr = oat.decode_step(ki.decode_x(w, [b])[0], L, ows, w.tau, caches, w.a, w.g, w.d_h, w.rope_base)[0]
         assert rel_err(to_np(y_all[b]), yr) <= 2e-2, b
     say("  chunks bit-identical to separate calls and to pages; oracle ok")
+
+
+def test_prefill_paged_full_size_stage():
+    """The 8-layer stage share (d_model 2048, 16 / 8 heads, B 4, S 4096) on scattered pages:
+    output and every producer's K/V bit-identical to the slot path."""
+    w = ki.stage_share_prefill()
+    B, S = w.batch, w.seq
+    stride = S // PAGE
+    say(f"[paged prefill full] {w.name}")
+    dm = build_device_model(w, B, S, w.kv_capacity)
+    tab, n_pages = scattered_table([S] * B, stride, 0, seed=11)
+    pools = make_pools(dm, n_pages)
+    tab_t = torch.from_numpy(tab).to(DEV)
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device=DEV)
+    kd.fill_prefill_x(w, x.data_ptr(), B, S)
+    y_c = torch.empty_like(x)
+    y_p = torch.full_like(x, float("nan"))
+    ws, n = workspace(dm, kb.KVP_PHASE_PREFILL, B, S)
+    st = torch.cuda.current_stream().cuda_stream
+    dm.model.kvp_prefill(x.data_ptr(), y_c.data_ptr(), B, S, ws.data_ptr(), n, st)
+    dm.model.kvp_prefill_paged(x.data_ptr(), y_p.data_ptr(), B, S, tab_t.data_ptr(), stride, ws.data_ptr(), n, st)
+    torch.cuda.synchronize()
+    assert torch.equal(y_c, y_p), "paged prefill differs from the slot path at full size"
+    for b in range(B):
+        got = gather(pools, tab_t, b, S)
+        for l, (K, V) in dm.slots.items():
+            assert torch.equal(got[l][0], K[b]), (b, l, "K")
+            assert torch.equal(got[l][1], V[b]), (b, l, "V")
+    say("  output and caches bit-identical to the slots")
+    del dm, pools, x, y_c, y_p, ws
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
