@@ -539,7 +539,7 @@ def main():
                     help="skip the achievable-peak calibration (no frac_achievable figures)")
     ap.add_argument("--no-train", action="store_true", help="skip the training-step line")
     ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib",
-                                       "train", "decode_capacity", "mall", "decode_graph"],
+                                       "train", "decode_capacity", "mall", "decode_graph", "prefill_paged"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain 1 GiB device copy (rocprofv3 counter calibration)")
@@ -581,6 +581,8 @@ def main():
             out = capacity_entry(steps_d, warm_d)
         elif args.only == "decode_graph":
             out = graph_entry(args.steps, args.warmup)
+        elif args.only == "prefill_paged":
+            out = paged_prefill_entry(args.steps, args.warmup)
         else:
             w = ki.stage_share_prefill()
             ms, prof, finite = bench_prefill(w, args.steps, args.warmup)
@@ -632,6 +634,7 @@ def main():
 
     if not args.no_extra:
         result["prefill_70b_stage"] = bench_70b(args.steps, args.warmup)
+        result["prefill_paged"] = paged_prefill_entry(args.steps, args.warmup)
 
     if not args.no_train:
         result["train"] = train_entry(w, max(3, args.steps // 2), max(1, args.warmup // 2))
@@ -821,6 +824,49 @@ def capacity_entry(steps: int, warmup: int, budget_gib: float = 160.0):
     out["paged_vs_slots_b8"] = {"paged_ms_per_step": round(ms_p, 4), "slots_ms_per_step": round(ms_s, 4),
                                 "ratio": round(ms_p / ms_s, 4)}
     log(f"[bench] 8-sequence ragged decode: pages {ms_p:.3f} ms, slots {ms_s:.3f} ms")
+    return out
+
+
+def paged_prefill_entry(steps: int, warmup: int):
+    """Cost of paging in prefill: the 8-layer stage share (B 4 x S 4096) on contiguous slots
+    and on pages (a seeded permutation of a pool of exactly the pages needed), same model."""
+    import torch
+    from kvp_inputs import device as kd
+    from paper_2608_15943_amd import binding as kb
+    w = ki.stage_share_prefill()
+    B, S = w.batch, w.seq
+    st = Stack(w, B, S, w.kv_capacity)
+    row = S // PAGE
+    n_pages = B * row
+    tab = torch.from_numpy(np.random.RandomState(1).permutation(n_pages).astype(np.int32).reshape(B, row)).cuda()
+    pools = []
+    for l in w.producers():
+        K = torch.empty((w.g, n_pages, PAGE, w.d_h), dtype=torch.bfloat16, device="cuda")
+        V = torch.empty((w.g, n_pages, w.d_h, PAGE), dtype=torch.bfloat16, device="cuda")
+        st.model.kvp_set_kv_pool(l, K.data_ptr(), V.data_ptr(), n_pages)
+        pools.append((K, V))
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device="cuda")
+    kd.fill_prefill_x(w, x.data_ptr(), B, S)
+    y = torch.empty_like(x)
+    yp = torch.empty_like(x)
+    n = st.model.kvp_workspace_size(kb.KVP_PHASE_PREFILL, B, S)
+    ws = torch.empty(n, dtype=torch.uint8, device="cuda")
+    cs = torch.cuda.current_stream().cuda_stream
+    ms_s, prof_s = time_steps(lambda: st.model.kvp_prefill(x.data_ptr(), y.data_ptr(), B, S, ws.data_ptr(), n, cs),
+                              st.model, steps, warmup)
+    ms_p, prof_p = time_steps(lambda: st.model.kvp_prefill_paged(x.data_ptr(), yp.data_ptr(), B, S, tab.data_ptr(),
+                                                                 row, ws.data_ptr(), n, cs),
+                              st.model, steps, warmup)
+    same = bool(torch.equal(y, yp))
+    avg = lambda prof, k: round(prof[k][1] / prof[k][0], 5)
+    out = {"workload": w.name, "slots_ms_per_step": round(ms_s, 4), "pages_ms_per_step": round(ms_p, 4),
+           "ratio": round(ms_p / ms_s, 4), "output_equal": same,
+           "kernels_avg_ms": {k: {"slots": avg(prof_s, k), "pages": avg(prof_p, k)}
+                              for k in ("qkv_gemm", "flash_attn", "oproj_gemm")}}
+    log(f"[bench] paged prefill {ms_p:.3f} ms vs slots {ms_s:.3f} ms (equal outputs: {same})")
+    del st, pools, x, y, yp, ws, tab
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
     return out
 
 
