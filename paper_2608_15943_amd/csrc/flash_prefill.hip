@@ -64,6 +64,10 @@ __device__ __forceinline__ void load_lds_1k(const void* gsrc, void* lds_base) {
     __builtin_amdgcn_global_load_lds((gvoid_t*)gsrc, (lvoid_t*)lds_base, 16, 0, 0);
 }
 
+// Word 3 of a raw buffer resource: a valid (32-bit) data format, so that dword loads are
+// range-checked against the record count and return zeros past it.
+constexpr int kRsrcWord3 = 0x00020000;
+
 __device__ __forceinline__ int swap_b23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
 
 // 8 waves of 32 queries; two waves per SIMD (<= 256 registers each), 128 KB of LDS.
@@ -117,6 +121,21 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
 
     const uint16_t* kbase = Kc + ((size_t)b * g + kvh) * cap * D;
     const uint16_t* vbase = Vc + ((size_t)b * g + kvh) * D * cap;
+    // Slots: one buffer resource per slot, sized to it, so a load past its end returns
+    // zeros without touching memory; per lane the offsets of its 4 + 4 loads are computed
+    // once and a tile adds t0 (one 32-bit add per load).
+    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kbase, 0, cap * D * 2, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vbase, 0, cap * D * 2, kRsrcWord3);
+    uint32_t koff[4], voff[4];
+    if constexpr (!PAGED) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+            const int r = 16 * wave + 4 * j + (lane >> 4);
+            const int c = (lane & 15) ^ (r & 15);
+            koff[j] = (uint32_t)(r * D + 8 * c) * 2u;
+            voff[j] = (uint32_t)(r * cap + 8 * c) * 2u;
+        }
+    }
 
     // Key tiles needed by this workgroup (causal, and never past S).
     const int last_q = min(qt * BQ + BQ - 1, S - 1);
@@ -158,13 +177,17 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             }
             return;
         }
+        // K rows t0 + r and V^T row r (dimension r), positions t0 + 8 c .. + 7.  Past the
+        // slot (only in the last tile when cap % 128 == 64) K rows read as zeros and V^T
+        // chunks read the next row's start: both lie beyond S, so their scores are masked
+        // and their V is zeroed.
+        const int wu = __builtin_amdgcn_readfirstlane(wave);   // LDS destinations are scalar
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
-            const int r = 16 * wave + 4 * j + (lane >> 4);
-            const int c = (lane & 15) ^ (r & 15);
-            load_lds_1k(kbase + (size_t)min(t0 + r, cap - 1) * D + 8 * c, &lk[stg][(16 * wave + 4 * j) * 16]);
-            const int cv = (lane & 15) ^ (r & 15);      // V^T row r = dimension r
-            load_lds_1k(vbase + (size_t)r * cap + min(t0 + 8 * cv, cap - 8), &lv[stg][(16 * wave + 4 * j) * 16]);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(krs, (lvoid_t*)&lk[stg][(16 * wu + 4 * j) * 16], 16,
+                                                     koff[j] + (uint32_t)t0 * (D * 2), 0, 0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(vrs, (lvoid_t*)&lv[stg][(16 * wu + 4 * j) * 16], 16,
+                                                     voff[j] + (uint32_t)t0 * 2, 0, 0, 0);
         }
     };
     auto fix_tail = [&](int t, int stg) {
@@ -193,8 +216,11 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
         __syncthreads();
     }
 
-    for (int t = 0; t < ntiles; ++t) {
-        const int stg = t & 1;
+    // One tile, with its LDS stage as a compile-time constant: the two stages are 32 KB
+    // apart, so every fragment address of stage 1 is stage 0's plus an immediate offset and
+    // the per-lane addresses are computed once for the whole loop.
+    auto tile = [&](int t, auto stg_t) {
+        constexpr int stg = decltype(stg_t)::value;
         const bool more = t + 1 < ntiles;
         bool issued = false;
 
@@ -234,13 +260,14 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
             issued = true;
             // Register i of block mb holds position t0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
             if constexpr (kDiag) {
+                // Visible: pos <= q_lane and pos < S, i.e. the register's offset within the
+                // lane's positions is at most lim (one compare against a constant each).
+                const int lim = min(q_lane, S - 1) - t0 - 8 * hi;
 #pragma unroll
                 for (int mb = 0; mb < 4; ++mb)
 #pragma unroll
-                    for (int i = 0; i < 16; ++i) {
-                        const int pos = t0 + 32 * mb + 16 * (i >> 3) + 8 * hi + (i & 7);
-                        if (pos > q_lane || pos >= S) s[mb][i] = -INFINITY;
-                    }
+                    for (int i = 0; i < 16; ++i)
+                        if (32 * mb + 16 * (i >> 3) + (i & 7) > lim) s[mb][i] = -INFINITY;
             }
             // ---- online softmax -------------------------------------------------------
             float mx = -INFINITY;
@@ -304,6 +331,10 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 __syncthreads();
             }
         }
+    };
+    for (int t = 0; t < ntiles; t += 2) {
+        tile(t, std::integral_constant<int, 0>{});
+        if (t + 1 < ntiles) tile(t + 1, std::integral_constant<int, 1>{});
     }
 
     // ---- normalise and store O[b, q, head, :] -------------------------------------
