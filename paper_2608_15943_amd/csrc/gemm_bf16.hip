@@ -27,6 +27,9 @@ namespace {
 
 constexpr int BM = 256, BN = 256, BK = 64, NT = 256, GROUP_M = 8;
 
+// Word 3 of a raw buffer resource: a valid (32-bit) data format.
+constexpr int kRsrcWord3 = 0x00020000;
+
 __device__ __forceinline__ const uint16_t* w_row(const WRows& w, int n, int K) {
     if (n < w.rows[0]) return (const uint16_t*)w.p[0] + (size_t)n * K;
     n -= w.rows[0];
@@ -354,7 +357,11 @@ typedef __attribute__((address_space(3))) void lvoid_t;
 // rows of one chunk column over all 64 banks.
 __device__ __forceinline__ int swz(int r, int c) { return c ^ ((r >> 1) & 7); }
 
-template <class Epi>
+// BUF: operand tiles are fetched with buffer loads into LDS, each lane's 8 + 8 offsets
+// computed once and the k-tile advance given as the scalar offset, so issuing a tile costs
+// no vector instructions (operands below 2 GiB; a wave's 64 W rows lie in one weight block
+// since block sizes and N are multiples of 128).
+template <class Epi, bool BUF>
 __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict__ A, WRows W,
                                                      int M, int N, int K, int splits, Epi epi) {
     __shared__ u32x4 lds[2][2][BM * 8];  // [stage][A, W][row * 8 + swizzled chunk]
@@ -380,20 +387,54 @@ __global__ __launch_bounds__(NT, 1) void gemm_bf16_nt(const uint16_t* __restrict
     // 64 w + 8 j + l / 8 and fetches the global chunk that belongs at LDS position l % 8.
     const uint16_t* a_src[8];
     const uint16_t* w_src[8];
+    uint32_t ga_off[8], gw_off[8];
+    __amdgpu_buffer_rsrc_t ars, wrs;
+    if constexpr (BUF) {
+        const int wu = __builtin_amdgcn_readfirstlane(wave);
+        ars = __builtin_amdgcn_make_buffer_rsrc((void*)A, 0, M * K * 2, kRsrcWord3);
+        const int x = n0 + 64 * wu;              // tile row 64 w (past N if the wave has no real row)
+        int nb = min(x, N - 1), blk = 0;
+        if (nb >= W.rows[0]) {
+            nb -= W.rows[0];
+            blk = 1;
+            if (nb >= W.rows[1]) {
+                nb -= W.rows[1];
+                blk = 2;
+            }
+        }
+        const int rows_blk = W.rows[blk];
+        wrs = __builtin_amdgcn_make_buffer_rsrc((void*)W.p[blk], 0, rows_blk * K * 2, kRsrcWord3);
+        const int nrow0 = nb + (x - min(x, N - 1));   // block row of tile row 64 w (rows past the block clamp)
 #pragma unroll
-    for (int j = 0; j < 8; ++j) {
-        const int row = 64 * wave + 8 * j + (lane >> 3);
-        const int c = swz(row, lane & 7);
-        a_src[j] = A + (size_t)min(m0 + row, M - 1) * K + kofs + 8 * c;
-        w_src[j] = w_row(W, min(n0 + row, N - 1), K) + kofs + 8 * c;
+        for (int j = 0; j < 8; ++j) {
+            const int row = 64 * wave + 8 * j + (lane >> 3);
+            const int c = swz(row, lane & 7);
+            ga_off[j] = (uint32_t)(min(m0 + row, M - 1) * K + kofs + 8 * c) * 2u;
+            gw_off[j] = (uint32_t)(min(nrow0 + 8 * j + (lane >> 3), rows_blk - 1) * K + kofs + 8 * c) * 2u;
+        }
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            const int row = 64 * wave + 8 * j + (lane >> 3);
+            const int c = swz(row, lane & 7);
+            a_src[j] = A + (size_t)min(m0 + row, M - 1) * K + kofs + 8 * c;
+            w_src[j] = w_row(W, min(n0 + row, N - 1), K) + kofs + 8 * c;
+        }
     }
     // Row group j (8 rows of A and of W) of tile kt into stage stg.
     auto issue_part = [&](int kt, int stg, int j) {
-        const int r0 = 64 * wave + 8 * j;
-        __builtin_amdgcn_global_load_lds((gvoid_t*)(a_src[j] + kt * BK), (lvoid_t*)&lds[stg][0][r0 * 8], 16,
-                                         0, 0);
-        __builtin_amdgcn_global_load_lds((gvoid_t*)(w_src[j] + kt * BK), (lvoid_t*)&lds[stg][1][r0 * 8], 16,
-                                         0, 0);
+        const int r0 = 64 * (BUF ? __builtin_amdgcn_readfirstlane(wave) : wave) + 8 * j;
+        if constexpr (BUF) {
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(ars, (lvoid_t*)&lds[stg][0][r0 * 8], 16, ga_off[j], kt * BK * 2,
+                                                     0, 0);
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(wrs, (lvoid_t*)&lds[stg][1][r0 * 8], 16, gw_off[j], kt * BK * 2,
+                                                     0, 0);
+        } else {
+            __builtin_amdgcn_global_load_lds((gvoid_t*)(a_src[j] + kt * BK), (lvoid_t*)&lds[stg][0][r0 * 8], 16,
+                                             0, 0);
+            __builtin_amdgcn_global_load_lds((gvoid_t*)(w_src[j] + kt * BK), (lvoid_t*)&lds[stg][1][r0 * 8], 16,
+                                             0, 0);
+        }
     };
     auto issue = [&](int kt, int stg) {
 #pragma unroll
@@ -635,8 +676,14 @@ template <class Epi>
 hipError_t launch(const uint16_t* A, const WRows& W, int M, int N, int K, const Epi& epi,
                   hipStream_t st, int splits = 1) {
     const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
-    hipLaunchKernelGGL(gemm_bf16_nt<Epi>, dim3(tiles * splits), dim3(NT), 0, st, A, W, M, N, K, splits,
-                       epi);
+    bool buf = (int64_t)M * K * 2 < ((int64_t)1 << 31) && N % 128 == 0;
+    for (int i = 0; i < 3; ++i) buf = buf && (int64_t)W.rows[i] * K * 2 < ((int64_t)1 << 31) && W.rows[i] % 128 == 0;
+    if (buf)
+        hipLaunchKernelGGL((gemm_bf16_nt<Epi, true>), dim3(tiles * splits), dim3(NT), 0, st, A, W, M, N, K, splits,
+                           epi);
+    else
+        hipLaunchKernelGGL((gemm_bf16_nt<Epi, false>), dim3(tiles * splits), dim3(NT), 0, st, A, W, M, N, K,
+                           splits, epi);
     return hipGetLastError();
 }
 
