@@ -160,3 +160,33 @@ def test_decode_128k_ragged_full_size():
     w = ki.decode_128k_ragged()
     lens = w.lengths()
     _decode_sample(w, lens, sample=int(np.argmin(lens)))
+
+
+def test_prefill_layer_with_operands_above_2gib():
+    """A 70B-shaped layer (d_model 8192, 64 / 8 heads) over B 16 x S 8192 = 131072 rows: its
+    projection input is 2 GiB, so the GEMMs take their global-load path instead of buffer
+    loads.  Positions [0, 64) of sequences 0 and 15 depend only on their own first 64
+    inputs (causal layer) and are compared with the oracle's 64-token problem."""
+    w0 = ki.stage_70b_prefill([0] * 10)
+    w = ki.Workload(**{**w0.__dict__, "L": 1, "tau": [0], "batch": 16, "seed": 120})
+    B, S, P = 16, w.seq, 64
+    assert B * S * w.h * 2 >= 2**31
+    say(f"[full] {w.name} one layer at B={B} S={S} (operands above 2 GiB)")
+    dm = build_device_model(w, B, S, w.kv_capacity)
+    ws_t, n = workspace(dm, kb.KVP_PHASE_PREFILL, B, S)
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device=DEV)
+    kd.fill_prefill_x(w, x.data_ptr(), B, S)
+    o = torch.empty((B, S, w.a * w.d_h), dtype=torch.bfloat16, device=DEV)
+    y = torch.empty_like(x)
+    dm.model.kvp_layer_forward(0, x.data_ptr(), o.data_ptr(), y.data_ptr(), B, S, ws_t.data_ptr(), n,
+                               torch.cuda.current_stream().cuda_stream)
+    torch.cuda.synchronize()
+    ow = oracle_weights(w)
+    for b in (0, B - 1):
+        xb = ki.prefill_x(w, [b], np.arange(P))[0]
+        yr, orf, _ = oat.layer_prefill(xb, ow[0], w.a, w.g, w.d_h, w.rope_base, shared_kv=None)
+        eo, ey = rel_err(to_np(o[b, :P]), orf), rel_err(to_np(y[b, :P]), yr)
+        say(f"  sequence {b}: attention output {eo:.3e}, layer output {ey:.3e}")
+        assert eo <= 2e-2 and ey <= 2e-2
+    del dm, ws_t, x, o, y
+    _release()
