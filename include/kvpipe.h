@@ -238,7 +238,7 @@ typedef struct kvp_model_desc {
     double rope_base;     /* RoPE base (> 0), e.g. 10000                             */
     int32_t max_batch;    /* largest B of any call, and the B extent of the KV slots */
     int32_t max_seq;      /* largest prefill S                                       */
-    int32_t kv_capacity;  /* positions per sequence in a KV slot; bf16: multiple of 64 */
+    int32_t kv_capacity;  /* positions per sequence in a KV slot; bf16: multiple of 64, < 2^23 */
     int32_t _pad;
 } kvp_model_desc;
 

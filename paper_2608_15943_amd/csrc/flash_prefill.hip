@@ -124,8 +124,9 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     // Slots: one buffer resource per slot, sized to it, so a load past its end returns
     // zeros without touching memory; per lane the offsets of its 4 + 4 loads are computed
     // once and a tile adds t0 (one 32-bit add per load).
-    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kbase, 0, cap * D * 2, kRsrcWord3);
-    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vbase, 0, cap * D * 2, kRsrcWord3);
+    const int slot_bytes = PAGED ? 0 : cap * D * 2;   // < 2^31: slots hold fewer than 2^23 positions
+    const __amdgpu_buffer_rsrc_t krs = __builtin_amdgcn_make_buffer_rsrc((void*)kbase, 0, slot_bytes, kRsrcWord3);
+    const __amdgpu_buffer_rsrc_t vrs = __builtin_amdgcn_make_buffer_rsrc((void*)vbase, 0, slot_bytes, kRsrcWord3);
     uint32_t koff[4], voff[4];
     if constexpr (!PAGED) {
 #pragma unroll

@@ -440,6 +440,8 @@ extern "C" int kvp_create(const kvp_model_desc* desc, const int32_t* tau, kvp_ct
         if (d.d_h != 128) return fail(KVP_E_SHAPE, "kvp_create: bf16 models need d_h == 128");
         if (d.kv_capacity % 64)
             return fail(KVP_E_SHAPE, "kvp_create: bf16 models need kv_capacity % 64 == 0");
+        if (d.kv_capacity >= (1 << 23))   // a slot's bytes fit a buffer resource's 32-bit size
+            return fail(KVP_E_SHAPE, "kvp_create: bf16 models need kv_capacity < 2^23");
         if (d.a / d.g > 16) return fail(KVP_E_SHAPE, "kvp_create: bf16 decode supports a / g <= 16");
     } else if (d.d_h != 16 && d.d_h != 32 && d.d_h != 64 && d.d_h != 128) {
         return fail(KVP_E_SHAPE, "kvp_create: fp32 models need d_h in {16, 32, 64, 128}");

@@ -214,6 +214,7 @@ def test_create_validates_shape_and_map():
                      (dict(tau=[0, 3, 2, 2]), kb.KVP_E_BAD_MAP),
                      (dict(d_h=64, a=4), kb.KVP_E_SHAPE),
                      (dict(kv_capacity=100), kb.KVP_E_SHAPE),
+                     (dict(kv_capacity=1 << 23), kb.KVP_E_SHAPE),
                      (dict(g=3), kb.KVP_E_INVALID_ARG),
                      (dict(h=300), kb.KVP_E_INVALID_ARG),
                      (dict(max_seq=256), kb.KVP_E_INVALID_ARG),
