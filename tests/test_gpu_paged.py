@@ -277,3 +277,46 @@ def test_prefill_paged_full_size_stage():
     del dm, pools, x, y_c, y_p, ws
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
+
+
+def test_unwritten_cache_contents_are_never_used():
+    """Cache memory past the written positions holds arbitrary bits in real use.  Slots and
+    pools filled with NaN before a prefill (S 300 in 512-position slots / 5-page rows) and the
+    decode step that follows give bit-identical results to zero-filled ones: positions >= S
+    (or > len_b) only ever meet masks that select, never multiply."""
+    w = small_workload("garbage-tail", 3, 512, 4, 2, [0, 0, 2], seed=34)
+    B, S, cap, stride = 2, 300, 512, 8
+    say(f"[garbage] B={B} S={S} cap={cap}")
+    outs = {}
+    for fill in (0.0, float("nan")):
+        dm = build_device_model(w, B, S, cap)
+        tab, n_pages = scattered_table([cap] * B, stride, 0, seed=12)
+        pools = make_pools(dm, n_pages)
+        for K, V in list(dm.slots.values()) + list(pools.values()):
+            K.fill_(fill)
+            V.fill_(fill)
+        tab_t = torch.from_numpy(tab).to(DEV)
+        x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device=DEV)
+        kd.fill_prefill_x(w, x.data_ptr(), B, S)
+        y = torch.empty_like(x)
+        yp = torch.empty_like(x)
+        ws, n = workspace(dm, kb.KVP_PHASE_PREFILL, B, S)
+        st = torch.cuda.current_stream().cuda_stream
+        dm.model.kvp_prefill(x.data_ptr(), y.data_ptr(), B, S, ws.data_ptr(), n, st)
+        dm.model.kvp_prefill_paged(x.data_ptr(), yp.data_ptr(), B, S, tab_t.data_ptr(), stride, ws.data_ptr(), n,
+                                   st)
+        xd = torch.empty((B, w.h), dtype=torch.bfloat16, device=DEV)
+        kd.fill_decode_x(w, xd.data_ptr(), B)
+        lens_t = torch.full((B,), S, dtype=torch.int32, device=DEV)
+        yd = torch.empty_like(xd)
+        ydp = torch.empty_like(xd)
+        wsd, nd = workspace(dm, kb.KVP_PHASE_DECODE, B)
+        dm.model.kvp_decode_step(xd.data_ptr(), lens_t.data_ptr(), S, yd.data_ptr(), B, wsd.data_ptr(), nd, st)
+        dm.model.kvp_decode_step_paged(xd.data_ptr(), lens_t.data_ptr(), S, tab_t.data_ptr(), stride,
+                                       ydp.data_ptr(), B, wsd.data_ptr(), nd, st)
+        torch.cuda.synchronize()
+        outs[fill == fill] = (y, yp, yd, ydp)
+        assert all(bool(torch.isfinite(t.float()).all().item()) for t in (y, yp, yd, ydp)), fill
+    for a, b in zip(outs[True], outs[False]):
+        assert torch.equal(a, b)
+    say("  NaN-filled caches give the zero-filled results bit for bit")
