@@ -222,3 +222,46 @@ def test_backward_stage_share_full_size_prefix():
     attends to); the bound here is 5e-2.  The three-layer test above holds the 2e-2 bar."""
     w = ki.stage_share_prefill()
     _prefix_case(w, w.batch, w.seq, 300, 5e-2, 5e-2)
+
+
+def _train_outputs(w, B, S, cap, fill):
+    dm = build_device_model(w, B, S, cap)
+    for K, V in dm.slots.values():
+        K.fill_(fill)
+        V.fill_(fill)
+    m = dm.model
+    st = torch.cuda.current_stream().cuda_stream
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device=DEV)
+    kd.fill_prefill_x(w, x.data_ptr(), B, S)
+    y = torch.empty_like(x)
+    ws, n = workspace(dm, kb.KVP_PHASE_PREFILL, B, S)
+    nsv = m.kvp_train_saved_size(B, S)
+    saved = torch.empty(nsv, dtype=torch.uint8, device=DEV)
+    m.kvp_train_forward(x.data_ptr(), y.data_ptr(), B, S, saved.data_ptr(), nsv, ws.data_ptr(), n, st)
+    outs = [y]
+    for l in range(w.L):
+        prod = w.tau[l] == l
+        g = [torch.empty((w.a * w.d_h, w.h), device=DEV), torch.empty((w.g * w.d_h, w.h), device=DEV) if prod else None,
+             torch.empty((w.g * w.d_h, w.h), device=DEV) if prod else None, torch.empty((w.h, w.a * w.d_h), device=DEV)]
+        m.kvp_set_layer_grads(l, *[t.data_ptr() if t is not None else 0 for t in g])
+        outs += [t for t in g if t is not None]
+    dy = torch.empty((B, S, w.h), dtype=torch.float32, device=DEV)
+    kd.fill_prefill_dy(w, dy.data_ptr(), B, S)
+    dx = torch.empty_like(dy)
+    wsb, nb = workspace(dm, kb.KVP_PHASE_BACKWARD, B, S)
+    m.kvp_backward(x.data_ptr(), dy.data_ptr(), dx.data_ptr(), B, S, saved.data_ptr(), nsv, wsb.data_ptr(), nb, st)
+    torch.cuda.synchronize()
+    return outs + [dx]
+
+
+def test_backward_ignores_unwritten_slot_contents():
+    """Slots filled with NaN past the S written positions (S 200 in 512-position slots):
+    the training forward and backward give the zero-filled results bit for bit."""
+    w = small_workload("bwd-garbage", 3, 512, 4, 2, [0, 0, 2], seed=24)
+    say("[backward garbage] S=200 cap=512")
+    a = _train_outputs(w, 2, 200, 512, 0.0)
+    b = _train_outputs(w, 2, 200, 512, float("nan"))
+    for i, (u, v) in enumerate(zip(a, b)):
+        assert bool(torch.isfinite(v.float()).all().item()), i
+        assert torch.equal(u, v), i
+    say("  bit-identical")
