@@ -83,6 +83,36 @@ __global__ __launch_bounds__(256) void transpose_kernel(const uint16_t* __restri
     }
 }
 
+// The same for R, C multiples of 64 and 16-byte aligned rows: 16-byte global accesses (a
+// lane reads 8 elements of a row and writes 8 of a transposed row).
+__global__ __launch_bounds__(256) void transpose16_kernel(const uint16_t* __restrict__ in,
+                                                          uint16_t* __restrict__ out, size_t in_ld,
+                                                          size_t out_ld) {
+    __shared__ uint16_t t[64][65];
+    const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+    const int tid = threadIdx.x, seg = tid & 7, row = tid >> 3;   // 8 lanes per 64-element row
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int r = row + 32 * k;
+        const u32x4 v = *(const u32x4*)(in + (size_t)(r0 + r) * in_ld + c0 + 8 * seg);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+            t[r][8 * seg + 2 * e] = (uint16_t)(v[e] & 0xFFFFu);
+            t[r][8 * seg + 2 * e + 1] = (uint16_t)(v[e] >> 16);
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+        const int c = row + 32 * k;   // output row c0 + c holds input column c0 + c
+        u32x4 v;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+            v[e] = (uint32_t)t[8 * seg + 2 * e][c] | ((uint32_t)t[8 * seg + 2 * e + 1][c] << 16);
+        *(u32x4*)(out + (size_t)(c0 + c) * out_ld + r0 + 8 * seg) = v;
+    }
+}
+
 __global__ __launch_bounds__(256) void f32_to_bf16_kernel(const float* __restrict__ x,
                                                           uint16_t* __restrict__ y, size_t n) {
     for (size_t i = (size_t)blockIdx.x * 256 + threadIdx.x; i < n; i += (size_t)gridDim.x * 256)
@@ -507,8 +537,13 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
 hipError_t transpose_bf16(const uint16_t* in, uint16_t* out, int R, int C, size_t in_ld, size_t out_ld,
                           hipStream_t st) {
     if (R < 1 || C < 1) return hipSuccess;
-    hipLaunchKernelGGL(transpose_kernel, dim3((R + 63) / 64, (C + 63) / 64), dim3(256), 0, st, in, out, R, C,
-                       in_ld, out_ld);
+    const bool wide = R % 64 == 0 && C % 64 == 0 && in_ld % 8 == 0 && out_ld % 8 == 0 &&
+                      ((reinterpret_cast<uintptr_t>(in) | reinterpret_cast<uintptr_t>(out)) & 15) == 0;
+    if (wide)
+        hipLaunchKernelGGL(transpose16_kernel, dim3(R / 64, C / 64), dim3(256), 0, st, in, out, in_ld, out_ld);
+    else
+        hipLaunchKernelGGL(transpose_kernel, dim3((R + 63) / 64, (C + 63) / 64), dim3(256), 0, st, in, out, R, C,
+                           in_ld, out_ld);
     return hipGetLastError();
 }
 
