@@ -720,6 +720,13 @@ hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int
     return launch(a, W, M, N, K, OutEpi{c, 0, 0, true}, st);
 }
 
+hipError_t gemm_nt_out_splits(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits, float* part,
+                              hipStream_t st) {
+    if (splits < 1 || K % (BK * splits)) return hipErrorInvalidValue;
+    WRows W{{w, nullptr, nullptr}, {N, 0, 0}};
+    return launch(a, W, M, N, K, OutEpi{part, (size_t)M * N, 0, false}, st, splits);
+}
+
 int gemm_out_splits(int M, int N, int K) {
     const int tiles = ((M + BM - 1) / BM) * ((N + BN - 1) / BN);
     const int nkt = (K + BK - 1) / BK;

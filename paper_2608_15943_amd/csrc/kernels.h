@@ -64,6 +64,10 @@ int gemm_out_splits(int M, int N, int K);
 hipError_t gemm_kmajor_out_bf16(const uint16_t* a, int lda, const uint16_t* b, int ldb, int M, int N, int K,
                                 int splits, float* part, hipStream_t st);
 // C = a @ w^T in bf16 (a [M][K], w [N][K], K % 64 == 0), no fused work.
+// part[s][M][N] (fp32, s < splits) = the K slice s of a @ w^T (a [M][K], w [N][K], both
+// K-contiguous); K a multiple of 64 * splits.
+hipError_t gemm_nt_out_splits(const uint16_t* a, const uint16_t* w, int M, int N, int K, int splits, float* part,
+                              hipStream_t st);
 hipError_t gemm_out_bf16(const uint16_t* a, const uint16_t* w, int M, int N, int K, uint16_t* c,
                          hipStream_t st);
 

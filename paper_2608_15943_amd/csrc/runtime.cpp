@@ -575,6 +575,10 @@ namespace {
 
 int round64(int S) { return (S + 63) / 64 * 64; }
 
+// Token counts that are multiples of this take the row-major weight-gradient GEMMs on
+// transposed activations (64-wide K tiles times up to 8 split-K slices).
+constexpr int kTokGrain = 512;
+
 // Per-layer activations of kvp_train_forward, layer l at l * stride: Q (after RoPE), the
 // attention output O and the layer input X in the model dtype, and (bf16 models) the
 // log-sum-exp of the scores, which fp32 models recompute.
@@ -602,7 +606,8 @@ Saved saved_layout(const kvp_ctx& c, int B, int S) {
 
 // Workspace of kvp_backward.
 struct BwdWs {
-    size_t gb = 0, dO = 0, lse = 0, dsum = 0, dqkv = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, total = 0;
+    size_t gb = 0, dO = 0, lse = 0, dsum = 0, dqkv = 0, acc = 0, wot = 0, wst = 0, part = 0, rope = 0, ta = 0, tb = 0,
+           total = 0;
     size_t acc_plane = 0;          // floats of one dK or dV sum
     std::vector<int> acc_slot;     // per layer: index of its fp32 sum pair, or -1
 };
@@ -652,6 +657,12 @@ BwdWs bwd_layout(const kvp_ctx& c, int B, int S) {
     const int sc = kvp::gemm_out_splits((int)nq, (int)h, (int)M);
     w.part = take(std::max({(size_t)so * h * nq, (size_t)sp * np * h, (size_t)sc * nq * h}) * sizeof(float));
     w.rope = take((size_t)S * 64 * sizeof(float2));
+    // Token-major copies for the row-major weight-gradient GEMMs (token counts that are
+    // multiples of 512): G^T or [dQ|dK|dV]^T, and O^T or X^T.
+    if (M % kTokGrain == 0) {
+        w.ta = take(M * std::max(h, np) * 2);
+        w.tb = take(M * std::max(h, nq) * 2);
+    }
     w.total = off;
     return w;
 }
@@ -1083,9 +1094,22 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
                  return check_hip(kvp::attn_bwd_prep_bf16(dO, Ol, dsum, B, S, Sp, ctx->d.a, st), "attention backward D");
              })))
             return rc;
+        const bool nt = M % kTokGrain == 0;
+        uint16_t* ta = bp(w.ta);
+        uint16_t* tb = bp(w.tb);
         {
             const int s = kvp::gemm_out_splits(h, nq, M);
-            if ((rc = gemm([&] { return check_hip(kvp::gemm_kmajor_out_bf16(gb, h, Ol, nq, h, nq, M, s, part, st), "dW_O GEMM"); })))
+            if (nt) {
+                // dW_O = G^T O on the token-major copies (row-major GEMM, split K).
+                if ((rc = aux([&] {
+                         int r2 = check_hip(kvp::transpose_bf16(gb, ta, M, h, h, M, st), "transpose G");
+                         if (!r2) r2 = check_hip(kvp::transpose_bf16(Ol, tb, M, nq, nq, M, st), "transpose O");
+                         return r2;
+                     })))
+                    return rc;
+                if ((rc = gemm([&] { return check_hip(kvp::gemm_nt_out_splits(ta, tb, h, nq, M, s, part, st), "dW_O GEMM"); })))
+                    return rc;
+            } else if ((rc = gemm([&] { return check_hip(kvp::gemm_kmajor_out_bf16(gb, h, Ol, nq, h, nq, M, s, part, st), "dW_O GEMM"); })))
                 return rc;
             if ((rc = aux([&] {
                      return check_hip(kvp::reduce_planes(part, s, h, nq, Ly.dwo, h, nullptr, 0, nullptr, st), "dW_O sum");
@@ -1133,9 +1157,19 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         // dW_Q (| dW_K | dW_V) = [dQ | dK | dV]^T X_l (both K-major over the tokens).
         {
             const int s = kvp::gemm_out_splits(np, h, M);
-            if ((rc = gemm([&] {
-                     return check_hip(kvp::gemm_kmajor_out_bf16(dqkv, np, Xl, h, np, h, M, s, part, st), "dW_QKV GEMM");
-                 })))
+            if (nt) {
+                if ((rc = aux([&] {
+                         int r2 = check_hip(kvp::transpose_bf16(dqkv, ta, M, np, np, M, st), "transpose dQKV");
+                         if (!r2) r2 = check_hip(kvp::transpose_bf16(Xl, tb, M, h, h, M, st), "transpose X");
+                         return r2;
+                     })))
+                    return rc;
+                if ((rc = gemm([&] { return check_hip(kvp::gemm_nt_out_splits(ta, tb, np, h, M, s, part, st), "dW_QKV GEMM"); })))
+                    return rc;
+            } else if ((rc = gemm([&] {
+                            return check_hip(kvp::gemm_kmajor_out_bf16(dqkv, np, Xl, h, np, h, M, s, part, st),
+                                             "dW_QKV GEMM");
+                        })))
                 return rc;
             if ((rc = aux([&] {
                      return check_hip(kvp::reduce_planes(part, s, np, h, Ly.dwq, nq, Ly.dwk, producer ? nkv : 0,
