@@ -410,7 +410,12 @@ int kvp_pager_rows(const kvp_pager* p, const int32_t* seqs, int B, int32_t* out)
  * caller's x), and for bf16 models the row log-sum-exp of the scaled scores
  * ([B, a, Sp] fp32, log2 domain, Sp = S rounded up to 64; fp32 models
  * recompute it).  The producers' K/V slots hold what the forward wrote; the
- * backward reads them.
+ * backward reads them.  Layout: layer l's record starts at l * stride and holds,
+ * in this order and each starting on a 256-byte boundary, Q_l, O_l, X_l (its
+ * bytes are reserved, unwritten, for l = 0) and (bf16) the log-sum-exp;
+ * stride = the record's size rounded up to 256 bytes, and the buffer is
+ * L * stride bytes.  Callers may read these tensors after the forward (e.g. to
+ * check a layer against a reference fed the same X_l).
  *
  * The backward runs the layers last to first.  For layer l with producer
  * p = tau(l): dW_O = G^T O_l and dO = G W_O with G = dLoss/dX_{l+1}; the

@@ -95,24 +95,48 @@ class LayerWeights:
         self.wo = np.asarray(wo, dtype=np.float64)
 
 
+def project_qkv(x: np.ndarray, positions: Sequence[int], w: LayerWeights, a: int, g: int, d_h: int,
+                base: float, kv: bool = True):
+    """Eq. (1) for the rows x [n, h] at the given absolute positions, with RoPE on Q and K.
+
+    Returns (q [a, n, d_h], k [g, n, d_h] or None, v [g, n, d_h] or None); K and V are
+    computed only when ``kv`` is set (a producer).
+    """
+    q = apply_rope(_heads(x @ w.wq.T, a, d_h), positions, base)
+    if not kv:
+        return q, None, None
+    k = apply_rope(_heads(x @ w.wk.T, g, d_h), positions, base)
+    v = _heads(x @ w.wv.T, g, d_h)
+    return q, k, v
+
+
+def output_projection(x: np.ndarray, o: np.ndarray, w: LayerWeights) -> np.ndarray:
+    """The residual block output X + O W_O^T for rows x [n, h] and attention outputs o [n, a*d_h]."""
+    return x + o @ w.wo.T
+
+
 def layer_prefill(x: np.ndarray, w: LayerWeights, a: int, g: int, d_h: int, base: float,
-                  shared_kv: Optional[Tuple[np.ndarray, np.ndarray]] = None):
+                  shared_kv: Optional[Tuple[np.ndarray, np.ndarray]] = None,
+                  rows: Optional[Sequence[int]] = None):
     """One layer over one sequence x [S, h].
 
     Producer (shared_kv is None): Q, K, V from x (Eq. 1), RoPE on Q and K.
     Consumer: Q from x, K and V = the producer's post-RoPE K, V (Eq. 3).
-    Returns (x_next [S, h], o [S, a*d_h], (K, V) used, each [g, S, d_h]).
+    ``rows`` (default: all S positions) selects the query positions whose outputs are
+    computed; a producer still projects K and V at every position of x.
+    Returns (x_next [n, h], o [n, a*d_h], (K, V) used, each [g, S, d_h]) for the n
+    selected rows.
     """
     S = x.shape[0]
     pos = np.arange(S)
-    q = apply_rope(_heads(x @ w.wq.T, a, d_h), pos, base)
+    qpos = pos if rows is None else np.asarray(rows)
+    q, _, _ = project_qkv(x[qpos], qpos, w, a, g, d_h, base, kv=False)
     if shared_kv is None:
-        k = apply_rope(_heads(x @ w.wk.T, g, d_h), pos, base)
-        v = _heads(x @ w.wv.T, g, d_h)
+        _, k, v = project_qkv(x, pos, w, a, g, d_h, base)
     else:
         k, v = shared_kv
-    o = _merge(attention(q, k, v, pos, pos))
-    return x + o @ w.wo.T, o, (k, v)
+    o = _merge(attention(q, k, v, qpos, np.arange(k.shape[1])))
+    return output_projection(x[qpos], o, w), o, (k, v)
 
 
 def stack_prefill(x: np.ndarray, weights: Sequence[LayerWeights], tau: Sequence[int], a: int,

@@ -123,3 +123,29 @@ def run_prefill(dm: DeviceModel, B: int, S: int):
 def small_workload(name, L, h, a, g, tau, dtype="bf16", d_h=128, seed=0):
     return ki.Workload(name=name, L=L, h=h, a=a, g=g, d_h=d_h, dtype=dtype, tau=list(tau),
                        phase="prefill", batch=1, seq=1, seed=seed)
+
+
+def _align256(n: int) -> int:
+    return (n + 255) // 256 * 256
+
+
+def saved_views(w: ki.Workload, saved: torch.Tensor, B: int, S: int):
+    """Per-layer views of kvp_train_forward's `saved` buffer (bf16 models), in the layout
+    the C ABI documents: layer l at l * stride holds Q [B*S, a*d_h], O [B*S, a*d_h], the
+    layer input X [B*S, h] (l >= 1) and the row log-sum-exp [B, a, S rounded up to 64]."""
+    M, nq = B * S, w.a * w.d_h
+    q_off = 0
+    o_off = q_off + _align256(M * nq * 2)
+    x_off = o_off + _align256(M * nq * 2)
+    lse_off = x_off + _align256(M * w.h * 2)
+    stride = lse_off + _align256(B * w.a * ((S + 63) // 64 * 64) * 4)
+    assert stride * w.L == saved.numel(), (stride * w.L, saved.numel())
+    out = []
+    for l in range(w.L):
+        base = l * stride
+        out.append({
+            "q": saved[base + q_off: base + q_off + M * nq * 2].view(torch.bfloat16).view(B, S, nq),
+            "o": saved[base + o_off: base + o_off + M * nq * 2].view(torch.bfloat16).view(B, S, nq),
+            "x": saved[base + x_off: base + x_off + M * w.h * 2].view(torch.bfloat16).view(B, S, w.h),
+        })
+    return out

@@ -140,11 +140,12 @@ def test_backward_fp32_matches_oracle(h, a, g, d, tau, B, S):
 
 
 
-def _prefix_case(w, B, S, P, tol_dx, tol_w):
+def _prefix_case(w, B, S, P, tol_dx, tol_w, model=None):
     """Training step of workload w at (B, S) with dY zero past position P: the loss reads only
     outputs at positions < P, which depend only on inputs before P (causal stack), so every
     gradient equals that of the P-token problem, which the oracle solves for all sequences;
-    dX past P is exactly 0."""
+    dX past P is exactly 0.  `model` (optional): (dx list, grads) of the bf16-forward
+    precision model on the same problem; the GPU must then also lie within TOL of it."""
     say(f"[backward full] {w.name} L={w.L} B={B} S={S} tau={w.tau}, dY zero past {P}")
     dm = build_device_model(w, B, S, w.kv_capacity)
     m = dm.model
@@ -200,6 +201,12 @@ def _prefix_case(w, B, S, P, tol_dx, tol_w):
                 say(f"  layer {l} {k}: {e:.3e}")
                 e_w = max(e_w, e)
     say(f"  max rel err: dx {e_dx:.3e}, weight gradients {e_w:.3e}")
+    if model is not None:
+        m_dx = max(rel_err(to_np(dx[b, :P]), model[0][b]) for b in range(B))
+        m_w = max(rel_err(to_np(grads[l][k]), model[1][l][k]) for l in range(w.L)
+                  for k in ("dwq", "dwk", "dwv", "dwo") if model[1][l][k] is not None)
+        say(f"  against the bf16-forward model: dx {m_dx:.3e}, weight gradients {m_w:.3e}")
+        assert m_dx <= TOL and m_w <= TOL, (m_dx, m_w)
     del dm, x, y, saved, ws, wsb, dy, dx, grads
     torch.cuda.synchronize()
     torch.cuda.empty_cache()
@@ -217,12 +224,16 @@ def test_backward_full_size_three_layers():
 
 def test_backward_stage_share_full_size_prefix():
     """The 8-layer stage share itself, composed.  Its gradients are bounded by what bf16
-    forward activations allow: a CPU emulation that rounds Q, K, V, O and the layer inputs to
-    bf16 and is otherwise exact moves this problem's dX by up to 2.8e-2 and its weight
-    gradients by up to 3.5e-2 of max|ref| (the largest at position 0, which every query
-    attends to); the bound here is 5e-2.  The three-layer test above holds the 2e-2 bar."""
+    forward activations allow: the precision model of tests/bf16_emulation.py (the oracle with
+    the layer inputs, Q, K, V and O rounded to bf16, otherwise exact) moves this problem's dX
+    by 2.8e-2 and its weight gradients by 3.5e-2 of max|ref| (test_bf16_backward_bound.py
+    reproduces this on the CPU), so the bound against the exact oracle is 5e-2; against that
+    model the GPU is held to the 2e-2 bar.  The three-layer test above holds 2e-2 against the
+    exact oracle."""
+    from bf16_emulation import stage_share_prefix_gradients
     w = ki.stage_share_prefill()
-    _prefix_case(w, w.batch, w.seq, 300, 5e-2, 5e-2)
+    (model,) = stage_share_prefix_gradients(P=300, batch=w.batch, kinds=("bf16",))
+    _prefix_case(w, w.batch, w.seq, 300, 5e-2, 5e-2, model=model)
 
 
 def _train_outputs(w, B, S, cap, fill):

@@ -222,3 +222,27 @@ def test_decode_matches_prefill_row():
     for prod, (kn, vn) in new_kv.items():
         np.testing.assert_allclose(kn, caches_full[prod][0][:, p], rtol=1e-12, atol=1e-13)
         np.testing.assert_allclose(vn, caches_full[prod][1][:, p], rtol=1e-12, atol=1e-13)
+
+
+def test_selected_rows_match_brute_force_and_causal_prefix():
+    """layer_prefill on chosen query rows (producer and consumer) equals the brute-force
+    scalar loops at those rows; a causal prefix of the input gives the same rows."""
+    r = rng(9)
+    h, a, g, d, S, base = 8, 4, 2, 4, 11, 100.0
+    ws = _tiny_weights(r, 2, h, a, g, d, [0, 0])
+    x = r.normal(size=(S, h))
+    rows = [0, 3, 7, 10]
+    y_b, o_b, kv_b = _brute_layer(x, ws[0], a, g, d, base)
+    y, o, (k, v) = at.layer_prefill(x, ws[0], a, g, d, base, rows=rows)
+    np.testing.assert_allclose(y, y_b[rows], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(o, o_b[rows], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(k, np.array(kv_b[0]), rtol=1e-11, atol=1e-12)
+    x1 = r.normal(size=(S, h))
+    y1_b, o1_b, _ = _brute_layer(x1, ws[1], a, g, d, base, kv=kv_b)
+    y1, o1, _ = at.layer_prefill(x1, ws[1], a, g, d, base, shared_kv=(k, v), rows=rows)
+    np.testing.assert_allclose(o1, o1_b[rows], rtol=1e-11, atol=1e-12)
+    np.testing.assert_allclose(y1, y1_b[rows], rtol=1e-11, atol=1e-12)
+    # Rows below n depend only on the first n inputs (the causal mask).
+    n = 8
+    yp, op, _ = at.layer_prefill(x[:n], ws[0], a, g, d, base, rows=[0, 3, 7])
+    np.testing.assert_allclose(op, o_b[[0, 3, 7]], rtol=1e-11, atol=1e-12)
