@@ -12,6 +12,7 @@
 
 #include <algorithm>
 #include <cstdint>
+#include <cstdlib>
 #include <cstring>
 #include <vector>
 
@@ -93,6 +94,7 @@ struct kvp_ctx {
     std::vector<Layer> layers;
     int decode_waves = 1024;          // decode attention grid: SIMDs of the device
     bool prof = false;
+    bool debug_sync = false;          // KVP_DEBUG_SYNC: wait for and check every launch
     std::vector<ProfRec> recs;        // launches timed since the last read
     std::vector<hipEvent_t> pool;     // idle events for reuse
     ~kvp_ctx() {
@@ -179,10 +181,33 @@ hipError_t take_event(kvp_ctx* c, hipEvent_t* e) {
     return hipEventCreate(e);
 }
 
+const char* kind_name(int kind) {
+    static const char* names[KVP_NUM_KERNEL_KINDS] = {
+        "RoPE table", "projection GEMM", "flash attention", "output projection GEMM",
+        "decode projection GEMM", "decode RoPE + append", "decode attention", "decode combine",
+        "decode output projection", "fp32 RoPE", "fp32 attention", "backward GEMM",
+        "backward attention dK/dV", "backward attention dQ", "backward auxiliary kernel"};
+    return kind >= 0 && kind < KVP_NUM_KERNEL_KINDS ? names[kind] : "kernel";
+}
+
+// Debug mode (KVP_DEBUG_SYNC set when the context was created): after each launch, wait
+// for the stream and check for an error, so that a failing kernel is named by its own
+// call rather than by a later one.  Not for use under graph capture.
+int debug_check(const kvp_ctx* c, int kind, hipStream_t st) {
+    if (!c->debug_sync) return KVP_OK;
+    hipError_t e = hipStreamSynchronize(st);
+    if (e == hipSuccess) e = hipGetLastError();
+    if (e != hipSuccess) return fail(KVP_E_HIP, "%s (debug sync): %s", kind_name(kind), hipGetErrorString(e));
+    return KVP_OK;
+}
+
 // Runs launch(); when timing is on, brackets it with two events on st.
 template <class F>
 int timed(kvp_ctx* c, int kind, hipStream_t st, F&& launch) {
-    if (!c->prof) return launch();
+    if (!c->prof) {
+        const int rc = launch();
+        return rc ? rc : debug_check(c, kind, st);
+    }
     hipEvent_t a, b;
     int rc;
     if ((rc = check_hip(take_event(c, &a), "hipEventCreate"))) return rc;
@@ -194,7 +219,8 @@ int timed(kvp_ctx* c, int kind, hipStream_t st, F&& launch) {
     rc = launch();
     const int rc2 = check_hip(hipEventRecord(b, st), "hipEventRecord");
     c->recs.push_back({kind, a, b});
-    return rc ? rc : rc2;
+    if (rc || rc2) return rc ? rc : rc2;
+    return debug_check(c, kind, st);
 }
 
 int check_layers(const kvp_ctx* c, int lo, int hi, bool paged = false) {
@@ -439,7 +465,7 @@ extern "C" int kvp_create(const kvp_model_desc* desc, const int32_t* tau, kvp_ct
     if (d.dtype == KVP_DTYPE_BF16) {
         if (d.d_h != 128) return fail(KVP_E_SHAPE, "kvp_create: bf16 models need d_h == 128");
         if (d.kv_capacity % 64)
-            return fail(KVP_E_SHAPE, "kvp_create: bf16 models need kv_capacity % 64 == 0");
+            return fail(KVP_E_SHAPE, "kvp_create: bf16 models need kv_capacity %% 64 == 0");
         if (d.kv_capacity >= (1 << 23))   // a slot's bytes fit a buffer resource's 32-bit size
             return fail(KVP_E_SHAPE, "kvp_create: bf16 models need kv_capacity < 2^23");
         if (d.a / d.g > 16) return fail(KVP_E_SHAPE, "kvp_create: bf16 decode supports a / g <= 16");
@@ -453,6 +479,8 @@ extern "C" int kvp_create(const kvp_model_desc* desc, const int32_t* tau, kvp_ct
     if (!c) return fail(KVP_E_INVALID_ARG, "kvp_create: out of host memory");
     c->d = d;
     c->tau = std::move(canon);
+    const char* dbg = std::getenv("KVP_DEBUG_SYNC");
+    c->debug_sync = dbg && dbg[0] && std::strcmp(dbg, "0") != 0;
     c->layers.resize(d.L);
     // Decode attention runs one wave per SIMD of the device current now; without a
     // device (planning-only use) the MI355X's 256 CUs are assumed.

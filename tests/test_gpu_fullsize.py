@@ -142,9 +142,13 @@ def test_prefill_70b_stage_composed_teacher_forced():
       * output projection + residual: X_l + O_l W_O^T against X_{l+1};
       * the producer's cache rows against the oracle's K, V on x;
       * the whole layer: the oracle layer fed X_l, with K, V from the oracle's own
-        producer, against O_l and X_{l+1}, where softmax is not so close to one-hot that a
-        rounding of Q, K to bf16 can move a row's weight onto another key (reported for
-        every layer; required while the largest scaled logit stays below 64).
+        producer, against X_{l+1} (required for every layer) and O_l (reported for every
+        layer, required where the largest scaled logit of the last row is below 20:
+        rounding Q and K to bf16, as the bf16 path does before Q K^T, moves a logit s by
+        about |s| 2^-8, so past that the softmax weights of this ill-conditioned stack move
+        by more than the bar allows; measured 9.5e-3 at a largest logit of 17, 1.8e-2 at 23,
+        3.8e-2 at 40, 7e-2 at 110, while each step on the GPU's own operands stays within
+        6e-3 and X_{l+1} within 8e-3).
     The forward output equals kvp_prefill's bit for bit.
     """
     local = plan_70b_stage_map()
@@ -198,8 +202,9 @@ def test_prefill_70b_stage_composed_teacher_forced():
         say(f"  layer {l}: Q {eq:.3e}, attention {eo:.3e}, output {ey:.3e}; whole layer O {eol:.3e}, "
             f"X {eyl:.3e} (largest scaled logit of the last row {logit:.1f})")
         assert eq <= 2e-2 and eo <= 2e-2 and ey <= 2e-2
-        if logit < 64:
-            assert eol <= 2e-2 and eyl <= 2e-2
+        assert eyl <= 2e-2
+        if logit < 20:
+            assert eol <= 2e-2
         worst = max(worst, eq, eo, ey)
     say(f"  worst step error {worst:.3e}")
     del dm, ws_t, saved, x, y

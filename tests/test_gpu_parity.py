@@ -182,3 +182,32 @@ def test_identity_map_equals_unshared_run_of_same_weights():
     assert rel_err(to_np(y_ident[0]), ref_i) <= 2e-2
     assert rel_err(to_np(y_shared[0]), ref_s) <= 2e-2
     assert rel_err(to_np(y_shared[0]), to_np(y_ident[0])) > 1e-2
+
+
+def test_debug_sync_mode_gives_the_same_results():
+    """A context created with KVP_DEBUG_SYNC set waits for and checks every launch; prefill
+    and decode results are bit-identical to a normal context's."""
+    import os
+    w = small_workload("debug-sync", 3, 512, 4, 2, [0, 0, 2], seed=41)
+    B, S, cap = 2, 150, 256
+    outs = []
+    for flag in ("0", "1"):
+        os.environ["KVP_DEBUG_SYNC"] = flag
+        try:
+            dm = build_device_model(w, B, S, cap)
+        finally:
+            os.environ.pop("KVP_DEBUG_SYNC", None)
+        _, y = run_prefill(dm, B, S)
+        x = torch.empty((B, w.h), dtype=torch.bfloat16, device=DEV)
+        kd.fill_decode_x(w, x.data_ptr(), B)
+        yd = torch.empty_like(x)
+        lens = torch.tensor([S, S - 7], dtype=torch.int32, device=DEV)
+        ws_t, n = workspace(dm, kb.KVP_PHASE_DECODE, B)
+        dm.model.kvp_decode_step(x.data_ptr(), lens.data_ptr(), S, yd.data_ptr(), B, ws_t.data_ptr(), n,
+                                 torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        outs.append((y, yd, [t.clone() for kv in dm.slots.values() for t in kv]))
+    assert torch.equal(outs[0][0], outs[1][0]) and torch.equal(outs[0][1], outs[1][1])
+    for a_, b_ in zip(outs[0][2], outs[1][2]):
+        assert torch.equal(a_, b_)
+    say("  debug-sync results bit-identical")
