@@ -325,6 +325,26 @@ int kvp_layer_forward(kvp_ctx* ctx, int l, const void* x, void* attn_out, void* 
 int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len, void* y,
                     int B, void* ws, size_t ws_bytes, void* stream);
 
+/*
+ * kvp_decode_step_noalloc -- kvp_decode_step for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that forbid
+ * allocation): the same kernels and arithmetic (y and the appended K/V are bit-identical
+ * to kvp_decode_step's), with the workspace taken from a device array of the library
+ * instead of a caller buffer.  The caller still passes x, y, len_dev and the slots.
+ * The array holds 64 MiB (enough for kvp_workspace_size(KVP_PHASE_DECODE, B) at B <= 64
+ * and h <= 8192 with the decode kernels' split counts), one copy per GPU, held until the
+ * process ends; its address on a device is looked up on the first call there (that
+ * call is the only one that may touch the HIP runtime beyond kernel launches).  The call
+ * itself allocates nothing and issues kernel launches only.  All calls on one GPU share
+ * the array: calls that overlap in time on one GPU (other streams, other contexts, other
+ * threads) race on it and give undefined results; calls in sequence on one stream are
+ * safe, and nothing in the array needs to start at zero.
+ * Errors: as kvp_decode_step; KVP_E_WORKSPACE when the call's workspace exceeds the
+ * array; KVP_E_HIP when the array's address cannot be found on the current device.
+ */
+int kvp_decode_step_noalloc(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
+                            void* y, int B, void* stream);
+
 /* ======================================================================== */
 /* Paged KV storage (capacity-driven serving)                                 */
 /* ======================================================================== */

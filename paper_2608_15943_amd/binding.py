@@ -46,7 +46,7 @@ EXPORTS = [
     "kvp_train_saved_size", "kvp_train_forward", "kvp_set_layer_grads", "kvp_backward",
     "kvp_set_kv_pool", "kvp_page_bytes", "kvp_prefill_paged", "kvp_decode_step_paged",
     "kvp_pager_create", "kvp_pager_destroy", "kvp_pager_reserve", "kvp_pager_release",
-    "kvp_pager_free_pages", "kvp_pager_rows",
+    "kvp_pager_free_pages", "kvp_pager_rows", "kvp_decode_step_noalloc",
     # include/kvp_calib.h: achievable-peak calibration (measurement support)
     "kvp_calib_mfma_bf16", "kvp_calib_stream_read",
 ]
@@ -125,6 +125,7 @@ def lib() -> C.CDLL:
         "kvp_page_bytes": ([vp, C.POINTER(C.c_size_t)], i32),
         "kvp_prefill_paged": ([vp, vp, vp, i32, i32, vp, i32, vp, C.c_size_t, vp], i32),
         "kvp_decode_step_paged": ([vp, vp, vp, i32, vp, i32, vp, i32, vp, C.c_size_t, vp], i32),
+        "kvp_decode_step_noalloc": ([vp, vp, vp, i32, vp, i32, vp], i32),
         "kvp_pager_create": ([i32, i32, i32, C.POINTER(vp)], i32),
         "kvp_pager_destroy": ([vp], None),
         "kvp_pager_reserve": ([vp, i32, i32], i32),
@@ -300,6 +301,10 @@ class Model:
     def kvp_decode_step(self, x, len_dev, max_len, y, B, ws, ws_bytes, stream=0):
         _check(lib().kvp_decode_step(self.ctx, x, len_dev, max_len, y, B, ws, ws_bytes,
                                      stream or None), "kvp_decode_step")
+
+    def kvp_decode_step_noalloc(self, x, len_dev, max_len, y, B, stream=0):
+        _check(lib().kvp_decode_step_noalloc(self.ctx, x, len_dev, max_len, y, B, stream or None),
+               "kvp_decode_step_noalloc")
 
     def kvp_set_kv_pool(self, l, k, v, n_pages):
         _check(lib().kvp_set_kv_pool(self.ctx, l, k, v, n_pages), "kvp_set_kv_pool")

@@ -34,7 +34,7 @@ HOST_FLAGS = ["-O2", "-std=c++17", "-fPIC", "-ffp-contract=off", "-fno-fast-math
               "-I", CSRC, "-Wall"]
 
 HIP_SOURCES = ["gemm_bf16.hip", "flash_prefill.hip", "decode_attn.hip", "decode_gemm.hip",
-               "small_kernels.hip", "calib.hip", "attn_bwd.hip", "bwd_f32.hip"]
+               "small_kernels.hip", "calib.hip", "attn_bwd.hip", "bwd_f32.hip", "noalloc.hip"]
 HIP_HOST_SOURCES = ["runtime.cpp"]   # host code that calls the HIP runtime
 HOST_SOURCES = ["planner.cpp", "pager.cpp"]   # pure host C++, no HIP
 

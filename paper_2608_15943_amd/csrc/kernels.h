@@ -120,6 +120,12 @@ hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st);
 // Largest decode grid (waves); the combine keeps one weight per wave of a pair in LDS.
 constexpr int kMaxDecodeSplits = 4096;
 
+// Allocation-free decode: the device array behind kvp_decode_step_noalloc (one per GPU,
+// held until the process ends).  static_scratch returns its address on the current
+// device (looked up on the first call on that device) and its size.
+constexpr size_t kStaticScratchBytes = (size_t)64 << 20;
+hipError_t static_scratch(void** addr, size_t* bytes);
+
 // Partial-result slots the decode attention writes: one per (wave, pair) piece, at most
 // waves + B * g of them, r = a / g rows of decode_partial_floats() floats each.
 inline size_t decode_partial_floats() { return 132; }

@@ -861,6 +861,23 @@ extern "C" int kvp_decode_step(kvp_ctx* ctx, const void* x, const int32_t* len_d
     return decode_impl(ctx, x, len_dev, max_len, y, B, ws, ws_bytes, stream, nullptr);
 }
 
+extern "C" int kvp_decode_step_noalloc(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
+                                       void* y, int B, void* stream) {
+    if (!ctx) return fail(KVP_E_INVALID_ARG, "kvp_decode_step_noalloc: NULL ctx");
+    if (B < 1) return fail(KVP_E_INVALID_ARG, "kvp_decode_step_noalloc: B >= 1 required");
+    const size_t need = layout(*ctx, KVP_PHASE_DECODE, B, 1).total;
+    if (need > kvp::kStaticScratchBytes)
+        return fail(KVP_E_WORKSPACE,
+                    "kvp_decode_step_noalloc: this call needs %zu bytes of scratch, the static array holds %zu",
+                    need, kvp::kStaticScratchBytes);
+    void* ws = nullptr;
+    size_t n = 0;
+    int rc;
+    if ((rc = check_hip(kvp::static_scratch(&ws, &n), "kvp_decode_step_noalloc: static scratch address")))
+        return rc;
+    return decode_impl(ctx, x, len_dev, max_len, y, B, ws, n, stream, nullptr);
+}
+
 extern "C" int kvp_decode_step_paged(kvp_ctx* ctx, const void* x, const int32_t* len_dev, int max_len,
                                      const int32_t* pages, int pages_stride, void* y, int B, void* ws,
                                      size_t ws_bytes, void* stream) {

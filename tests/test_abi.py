@@ -415,3 +415,21 @@ def test_paged_entry_points_host_checks():
         f.kvp_set_kv_pool(0, fake, fake, 4)
     assert e.value.code == kb.KVP_E_SHAPE
     f.close()
+
+
+def test_noalloc_decode_rejects_workspace_beyond_the_static_array():
+    """kvp_decode_step_noalloc checks, before touching the GPU, that the call's workspace fits
+    the library's 64 MiB device array: a 70B-wide model (d_model 8192) fits at B = 64 and not
+    at B = 100; a NULL context or B < 1 is rejected as an argument error."""
+    m = kb.Model(1, 8192, 64, 8, 128, kb.KVP_DTYPE_BF16, [0], max_batch=128, max_seq=1, kv_capacity=128)
+    assert m.kvp_workspace_size(kb.KVP_PHASE_DECODE, 64) <= 64 << 20
+    assert m.kvp_workspace_size(kb.KVP_PHASE_DECODE, 100) > 64 << 20
+    fake = 1 << 20
+    with pytest.raises(kb.KvpError) as e:
+        m.kvp_decode_step_noalloc(fake, fake * 2, 10, fake * 4, 100)
+    assert e.value.code == kb.KVP_E_WORKSPACE
+    assert "static array" in kb.lib().kvp_last_error().decode()
+    with pytest.raises(kb.KvpError) as e:
+        m.kvp_decode_step_noalloc(fake, fake * 2, 10, fake * 4, 0)
+    assert e.value.code == kb.KVP_E_INVALID_ARG
+    assert kb.lib().kvp_decode_step_noalloc(None, fake, fake, 1, fake, 1, None) == kb.KVP_E_INVALID_ARG
