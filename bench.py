@@ -112,9 +112,10 @@ class Stack:
         from kvp_inputs import device as kd
         from paper_2608_15943_amd import binding as kb
         self.w, self.B, self.cap = w, B, cap
-        dt = torch.bfloat16
-        self.model = kb.Model(w.L, w.h, w.a, w.g, w.d_h, kb.KVP_DTYPE_BF16, w.tau, max_batch=B,
-                              max_seq=max_seq, kv_capacity=cap, rope_base=w.rope_base)
+        dt = torch.bfloat16 if w.dtype == "bf16" else torch.float32
+        self.model = kb.Model(w.L, w.h, w.a, w.g, w.d_h,
+                              kb.KVP_DTYPE_BF16 if w.dtype == "bf16" else kb.KVP_DTYPE_FP32, w.tau,
+                              max_batch=B, max_seq=max_seq, kv_capacity=cap, rope_base=w.rope_base)
         self.keep = []
         for l in range(w.L):
             prod = w.tau[l] == l
@@ -142,19 +143,28 @@ class Stack:
         torch.cuda.synchronize()
 
 
+LAST_STEP_MS = []   # per-step times (ms) of the last time_steps call
+
+
 def time_steps(run, model, steps: int, warmup: int):
     """Warm up, time exactly `steps` calls between two device synchronisations, then time
     another `steps` calls with the library's per-launch HIP events on (for the per-kernel
-    figures), so that the step time itself is not perturbed by the event records."""
+    figures), so that the step time itself is not perturbed by the event records.  The timed
+    calls are also separated by events on the launch stream (one record between calls), whose
+    per-step times are kept in LAST_STEP_MS for the spread of the step time."""
     import torch
     for _ in range(warmup):
         run()
     torch.cuda.synchronize()
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     t0 = time.perf_counter()
-    for _ in range(steps):
+    evs[0].record()
+    for i in range(steps):
         run()
+        evs[i + 1].record()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    LAST_STEP_MS[:] = [evs[i].elapsed_time(evs[i + 1]) for i in range(steps)]
     model.kvp_profile_enable(True)
     for _ in range(steps):
         run()
@@ -162,6 +172,14 @@ def time_steps(run, model, steps: int, warmup: int):
     prof = model.kvp_profile_read()
     model.kvp_profile_enable(False)
     return (t1 - t0) * 1e3 / steps, prof
+
+
+def step_spread():
+    """Min / median / max of the per-step times of the last time_steps call (ms)."""
+    t = sorted(LAST_STEP_MS)
+    if not t:
+        return None
+    return {"min": round(t[0], 4), "median": round(t[len(t) // 2], 4), "max": round(t[-1], 4)}
 
 
 def bench_prefill(w: ki.Workload, steps: int, warmup: int, tau=None):
@@ -172,7 +190,8 @@ def bench_prefill(w: ki.Workload, steps: int, warmup: int, tau=None):
         w = w.with_map(tau, "-identity")
     B, S = w.batch, w.seq
     st = Stack(w, B, S, w.kv_capacity)
-    x = torch.empty((B, S, w.h), dtype=torch.bfloat16, device="cuda")
+    x = torch.empty((B, S, w.h), dtype=torch.bfloat16 if w.dtype == "bf16" else torch.float32,
+                    device="cuda")
     kd.fill_prefill_x(w, x.data_ptr(), B, S)
     y = torch.empty_like(x)
     n = st.model.kvp_workspace_size(kb.KVP_PHASE_PREFILL, B, S)
@@ -538,7 +557,7 @@ def main():
     ap.add_argument("--no-calib", action="store_true",
                     help="skip the achievable-peak calibration (no frac_achievable figures)")
     ap.add_argument("--no-train", action="store_true", help="skip the training-step line")
-    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib",
+    ap.add_argument("--only", choices=["prefill", "prefill_70b", "decode", "decode_128k", "calib", "tiny",
                                        "train", "decode_capacity", "mall", "decode_graph", "prefill_paged"],
                     help="run one workload only and print its entry (for profiling)")
     ap.add_argument("--calibrate-copy", action="store_true",
@@ -579,6 +598,8 @@ def main():
             out = train_entry(ki.stage_share_prefill(), steps_d, warm_d)
         elif args.only == "decode_capacity":
             out = capacity_entry(steps_d, warm_d)
+        elif args.only == "tiny":
+            out = tiny_entry(args.steps, args.warmup)
         elif args.only == "decode_graph":
             out = graph_entry(args.steps, args.warmup)
         elif args.only == "prefill_paged":
@@ -633,7 +654,9 @@ def main():
         log(f"[bench] identity map {ms_u:.3f} ms/step (speedup {ms_u / ms:.4f}, ideal {ideal:.4f})")
 
     if not args.no_extra:
-        result["prefill_70b_stage"] = bench_70b(args.steps, args.warmup)
+        result["prefill_70b_stage"] = bench_70b(args.steps, args.warmup, unshared=not args.no_unshared,
+                                                cpu=not args.no_cpu)
+        result["tiny_fp32"] = tiny_entry(args.steps, args.warmup)
         result["prefill_paged"] = paged_prefill_entry(args.steps, args.warmup)
 
     if not args.no_train:
@@ -653,12 +676,39 @@ def main():
             wi = wd.with_map(list(range(wd.L)), "-identity")
             u = decode_entry(wi, steps_d, warm_d, alias_of={l: wd.tau[l] for l in range(wd.L)
                                                             if wd.tau[l] != l})
+            sh, un = result["decode"]["step_ms_spread"], u["step_ms_spread"]
             result["decode"]["shared_vs_unshared"] = {
                 "step_speedup": round(u["ms_per_step"] / result["decode"]["ms_per_step"], 4),
-                "unshared_ms_per_step": u["ms_per_step"],
+                "step_speedup_range": [round(un["min"] / sh["max"], 4), round(un["max"] / sh["min"], 4)],
+                "ideal": round(sum(decode_bytes(wi, wi.lengths()).values()) /
+                               sum(decode_bytes(wd, wd.lengths()).values()), 4),
+                "unshared_ms_per_step": u["ms_per_step"], "unshared_step_ms_spread": un,
+                "aliased": True,
+                "alias_map": {str(l): wd.tau[l] for l in range(wd.L) if wd.tau[l] != l},
+                "alias_note": "the 32 unshared caches (275 GB) do not fit beside the rest, so each "
+                              "former consumer's slot is the memory of its former producer's; every "
+                              "layer still appends and reads a full cache of its own length",
                 "kv_cache_bytes_shared": kv_bytes(wd), "kv_cache_bytes_unshared": kv_bytes(wi)}
         if not args.no_extra:
-            result["decode_ragged_128k"] = decode_entry(ki.decode_128k_ragged(), steps_d, warm_d)
+            w4 = ki.decode_128k_ragged()
+            result["decode_ragged_128k"] = decode_entry(w4, steps_d, warm_d)
+            if not args.no_unshared:
+                # Identity map: all 32 layers own a cache (137 GB at 128K capacity, fits).
+                w4i = w4.with_map(list(range(w4.L)), "-identity")
+                u4 = decode_entry(w4i, steps_d, warm_d)
+                sh, un = result["decode_ragged_128k"]["step_ms_spread"], u4["step_ms_spread"]
+                result["decode_ragged_128k"]["shared_vs_unshared"] = {
+                    "step_speedup": round(u4["ms_per_step"] / result["decode_ragged_128k"]["ms_per_step"], 4),
+                    "step_speedup_range": [round(un["min"] / sh["max"], 4), round(un["max"] / sh["min"], 4)],
+                    "ideal": round(sum(decode_bytes(w4i, w4i.lengths()).values()) /
+                                   sum(decode_bytes(w4, w4.lengths()).values()), 4),
+                    "unshared_ms_per_step": u4["ms_per_step"], "unshared_step_ms_spread": un,
+                    "aliased": False,
+                    "kv_cache_bytes_shared": kv_bytes(w4), "kv_cache_bytes_unshared": kv_bytes(w4i)}
+            if not args.no_cpu:
+                log("[bench] oracle CPU baseline (ragged 128K decode, the shortest sequence)")
+                l4 = w4.lengths()
+                result["decode_ragged_128k"]["cpu_baseline"] = cpu_baseline_decode(w4, l4, int(np.argmin(l4)))
             result["decode_capacity"] = capacity_entry(steps_d, warm_d)
             result["decode_graph"] = graph_entry(args.steps, args.warmup)
 
@@ -666,7 +716,41 @@ def main():
         log(f"[bench] oracle CPU baseline ({args.cpu_seq} positions of one sequence)")
         result["cpu_baseline"] = cpu_baseline(w, args.cpu_seq)
 
+    result["workloads"] = workload_table(result)
     print(json.dumps(result), flush=True)
+
+
+def workload_table(r):
+    """One row per workload of the run: step time, rate, roofline fraction of the dominant
+    kernel, shared-vs-unshared ratio and the oracle's rate, gathered from the entries above."""
+    def cpu(e):
+        c = e.get("cpu_baseline")
+        return None if not c else {"value": c["value"], "unit": c["unit"], "cores": c["cores"],
+                                   **({"extrapolated": True} if c.get("extrapolated") else {})}
+    rows = {r["config"]["workload"]: {
+        "ms_per_step": r["ms_per_step"], "rate": r["value"], "unit": r["unit"],
+        "roofline_frac": r["roofline"]["frac"], "roofline_kernel": r["roofline"]["kernel"],
+        "shared_vs_unshared": (r.get("shared_vs_unshared") or {}).get("prefill_speedup"), "cpu_baseline": cpu(r)}}
+    if "tiny_fp32" in r:
+        e = r["tiny_fp32"]
+        rows[e["workload"]] = {"ms_per_step": e["ms_per_step"], "rate": e["tflops"], "unit": "TFLOP/s",
+                               "roofline_frac": None, "roofline_kernel": "launch-bound: time only",
+                               "shared_vs_unshared": None, "cpu_baseline": cpu(e)}
+    if "prefill_70b_stage" in r:
+        e = r["prefill_70b_stage"]
+        rows[e["workload"]] = {"ms_per_step": e["ms_per_step"], "rate": e["tflops"], "unit": "TFLOP/s",
+                               "roofline_frac": e["roofline"]["frac"], "roofline_kernel": e["roofline"]["kernel"],
+                               "shared_vs_unshared": (e.get("shared_vs_unshared") or {}).get("prefill_speedup"),
+                               "cpu_baseline": cpu(e)}
+    for k in ("decode", "decode_ragged_128k"):
+        if k in r:
+            e = r[k]
+            rows[e["workload"]] = {"ms_per_step": e["ms_per_step"], "rate": e["tokens_per_s"], "unit": "tokens/s",
+                                   "hbm_gbs": e["hbm_gbs"], "hbm_frac": e["hbm_frac"],
+                                   "roofline_frac": e["roofline"]["frac"], "roofline_kernel": e["roofline"]["kernel"],
+                                   "shared_vs_unshared": (e.get("shared_vs_unshared") or {}).get("step_speedup"),
+                                   "cpu_baseline": cpu(e)}
+    return rows
 
 
 def kv_bytes(w: ki.Workload) -> int:
@@ -677,6 +761,7 @@ def kv_bytes(w: ki.Workload) -> int:
 def decode_entry(wd: ki.Workload, steps: int, warmup: int, alias_of=None):
     log(f"[bench] decode {wd.name}")
     dms, dprof, dfin, lens = bench_decode(wd, steps, warmup, alias_of=alias_of)
+    spread = step_spread()
     db = decode_bytes(wd, lens)
     dtotal = sum(db.values())
     n_a = dprof["dec_attn"][0]
@@ -687,7 +772,8 @@ def decode_entry(wd: ki.Workload, steps: int, warmup: int, alias_of=None):
     out = {
         "workload": wd.name, "batch": wd.batch, "context": [int(lens.min()), int(lens.max())],
         "map": wd.tau, "tokens_per_s": round(wd.batch / (dms * 1e-3), 2),
-        "ms_per_step": round(dms, 4), "hbm_gbs": round(dtotal / (dms * 1e-3) / 1e9, 1),
+        "ms_per_step": round(dms, 4), "step_ms_spread": spread,
+        "hbm_gbs": round(dtotal / (dms * 1e-3) / 1e9, 1),
         "hbm_frac": round(dtotal / (dms * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
         "hbm_frac_achievable": (round(dtotal / (dms * 1e-3) / 1e9 / ACHIEVABLE["hbm_read_gbs"], 4)
                                 if ACHIEVABLE.get("hbm_read_gbs") else None),
@@ -928,10 +1014,11 @@ def graph_entry(steps: int, warmup: int, B: int = 8, ctx: int = 4096):
     return out
 
 
-def bench_70b(steps: int, warmup: int):
+def bench_70b(steps: int, warmup: int, unshared: bool = False, cpu: bool = False):
     """The 70B-shaped stage: its map comes from the C++ planner (Algorithm 1) on the
     stage-tail-heavy synthetic FLOPs of 80 layers over 8 stages, each stage's first layer
-    kept; the stage run on this GPU is the last one."""
+    kept; the stage run on this GPU is the last one.  unshared: also time the identity map
+    (every layer a producer); cpu: the oracle on a layer subset (see cpu_baseline_70b)."""
     from paper_2608_15943_amd import binding as kb
     Lw = 80
     t0 = time.perf_counter()
@@ -945,6 +1032,7 @@ def bench_70b(steps: int, warmup: int):
     log(f"[bench] prefill {w5.name} map {local} (planner {plan_us:.0f} us, FIR {plan['fir']:.4f})")
     steps5 = max(3, steps // 2)
     ms5, prof5, fin5 = bench_prefill(w5, steps5, max(1, warmup // 2))
+    spread5 = step_spread()
     fl5 = prefill_flops(w5, w5.batch, w5.seq)
     dom5 = max(("qkv_gemm", "flash_attn", "oproj_gemm"), key=lambda k: prof5.get(k, (0, 0.0))[1])
     rl = roofline_entry(dom5, prof5, fl5[dom5] / w5.L, w5.L * steps5 / prof5[dom5][0],
@@ -954,13 +1042,79 @@ def bench_70b(steps: int, warmup: int):
                                                           "n_converted": plan["n_converted"],
                                                           "host_us": round(plan_us, 1)},
            "tflops": round(sum(fl5.values()) / (ms5 * 1e-3) / 1e12, 2),
-           "ms_per_step": round(ms5, 4), "finite": fin5, "roofline": rl,
+           "ms_per_step": round(ms5, 4), "step_ms_spread": spread5, "finite": fin5, "roofline": rl,
            "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof5.items()},
            "per_kernel_tflops": {k: round(fl5[k] * steps5 / prof5[k][1] / 1e9, 1)
                                  for k in fl5 if k in prof5}}
     out["per_kernel_roofline"] = kernel_fracs(out["per_kernel_tflops"])
     log(f"[bench] 70B stage {ms5:.3f} ms/step, {out['tflops']} TFLOP/s")
+    if unshared:
+        ident = list(range(w5.L))
+        ms_u, _, _ = bench_prefill(w5, steps5, max(1, warmup // 2), tau=ident)
+        sp_u = step_spread()
+        ideal = sum(prefill_flops(w5, w5.batch, w5.seq, ident).values()) / sum(fl5.values())
+        out["shared_vs_unshared"] = {"prefill_speedup": round(ms_u / ms5, 4), "prefill_ideal": round(ideal, 4),
+                                     "speedup_range": [round(sp_u["min"] / spread5["max"], 4),
+                                                       round(sp_u["max"] / spread5["min"], 4)],
+                                     "unshared_ms_per_step": round(ms_u, 4)}
+        log(f"[bench] 70B stage identity map {ms_u:.3f} ms/step (speedup {ms_u / ms5:.4f}, ideal {ideal:.4f})")
+    if cpu:
+        log("[bench] oracle CPU baseline (70B-shaped stage, layer subset)")
+        out["cpu_baseline"] = cpu_baseline_70b(w5)
     return out
+
+
+def cpu_baseline_70b(w5: ki.Workload, s_sample: int = 2048):
+    """The oracle on a bounded sample of the 70B-shaped stage: its producer (layer 0) and one
+    consumer (the last layer, fed the producer's output and reading its K, V) over the first
+    s_sample positions of the sequence (a causal prefix is an exact sample of those rows).
+    The rate is the sample's algorithmic FLOPs over the oracle's time; applied to the whole
+    stage it extrapolates (the oracle's attention cost grows with the sequence length)."""
+    from oracle import attention as oat
+    threads, host = host_info()
+    sub = ki.Workload(**{**w5.__dict__, "L": 2, "tau": [0, 0]})
+    wts = [oat.LayerWeights(ki.weight(w5, ki.KIND_WQ, 0), ki.weight(w5, ki.KIND_WK, 0),
+                            ki.weight(w5, ki.KIND_WV, 0), ki.weight(w5, ki.KIND_WO, 0)),
+           oat.LayerWeights(ki.weight(w5, ki.KIND_WQ, w5.L - 1), None, None,
+                            ki.weight(w5, ki.KIND_WO, w5.L - 1))]
+    x = ki.prefill_x(w5, [0], np.arange(s_sample))[0]
+    t0 = time.perf_counter()
+    oat.stack_prefill(x, wts, [0, 0], w5.a, w5.g, w5.d_h, w5.rope_base)
+    dt = time.perf_counter() - t0
+    flops = sum(prefill_flops(sub, 1, s_sample).values())
+    rate = flops / dt
+    return {"value": round(rate / 1e12, 6), "unit": "TFLOP/s", "cores": threads, "kind": "oracle",
+            "sample": (f"layers 0 (producer) and {w5.L - 1} (consumer of layer 0) on positions "
+                       f"[0, {s_sample}) of the sequence, fp64 NumPy with host BLAS; {dt:.1f} s"),
+            "extrapolated": True,
+            "extrapolated_ms_per_step": round(sum(prefill_flops(w5, w5.batch, w5.seq).values()) / rate * 1e3, 1),
+            "host": host}
+
+
+def tiny_entry(steps: int, warmup: int):
+    """The tiny fp32 stack (4 layers, d_model 256, 4 x 64 heads, S 128, map [0, 0, 2, 2]): every
+    step on the vector ALUs in fp32; launch-bound, so only its time is reported (no roofline),
+    next to the oracle's time for the same stack on the host."""
+    from oracle import attention as oat
+    w = ki.tiny_fp32()
+    ms, prof, fin = bench_prefill(w, steps, warmup)
+    fl = sum(prefill_flops(w, w.batch, w.seq).values())
+    threads, host = host_info()
+    wts = oracle_weights(w)
+    x = ki.prefill_x(w, [0], np.arange(w.seq))[0]
+    reps = 20
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        oat.stack_prefill(x, wts, w.tau, w.a, w.g, w.d_h, w.rope_base)
+    dt = (time.perf_counter() - t0) / reps
+    return {"workload": w.name, "dtype": "f32", "ms_per_step": round(ms, 4), "step_ms_spread": step_spread(),
+            "tflops": round(fl / (ms * 1e-3) / 1e12, 4), "flops_per_step": fl, "finite": fin,
+            "bound": "launch", "launches_per_step": sum(n for n, _ in prof.values()) // max(1, steps),
+            "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof.items()},
+            "cpu_baseline": {"value": round(fl / dt / 1e12, 6), "unit": "TFLOP/s", "cores": threads,
+                             "kind": "oracle", "ms_per_step": round(dt * 1e3, 3),
+                             "sample": f"the whole stack (sequence of {w.seq}), fp64 NumPy, mean of {reps} runs",
+                             "host": host}}
 
 
 if __name__ == "__main__":
