@@ -44,6 +44,7 @@
 // heaviest-first list instead put all the long tiles on the first XCDs: 1.4x
 // slower on the 8-layer stage share.)
 #include <math.h>
+#include <stdint.h>
 #include <type_traits>
 
 #include "common.h"
@@ -69,6 +70,24 @@ __device__ __forceinline__ void load_lds_1k(const void* gsrc, void* lds_base) {
 constexpr int kRsrcWord3 = 0x00020000;
 
 __device__ __forceinline__ int swap_b23(int r) { return (r & ~12) | ((r & 4) << 1) | ((r & 8) >> 1); }
+
+// LDS fragment reads with their waits placed by hand.  The compiler, at this kernel's register
+// pressure, issues the next fragment read right before the MFMA that needs it and waits for it
+// there, so every fragment's LDS latency stalls the wave.  These reads go ahead by two k steps
+// (three rotating sets of four fragments) and each step waits only for its own set: the
+// reads return in order and nothing else uses the LDS counter inside those loops.  A wait
+// names the set it completes as an in/out operand, so the MFMAs that read the set cannot be
+// scheduled before it.
+template <int OFF>
+__device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+    return v;
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait(u32x4 (&f)[4]) {
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(f[0]), "+v"(f[1]), "+v"(f[2]), "+v"(f[3]) : "i"(N));
+}
 
 // 8 waves of 32 queries; two waves per SIMD (<= 256 registers each), 128 KB of LDS.
 template <bool PAGED>
@@ -209,6 +228,15 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     float m_run = -INFINITY, l_run = 0.f;
 
     const int ksw = swap_b23(l32);          // K row read by this lane inside a 32-row block
+    // LDS byte addresses of this lane's fragments in stage 0: K step ks of block 0 (block mb is
+    // 8 KB further, since rows 32 mb + ksw share ksw's swizzle) and V^T chunk c of d block 0
+    // (d blocks are 8 KB apart likewise); stage 1 is 32 KB further.
+    uint32_t kaddr[8], vaddr[8];
+#pragma unroll
+    for (int ks = 0; ks < 8; ++ks) {
+        kaddr[ks] = (uint32_t)(uintptr_t)&lk[0][ksw * 16 + ((2 * ks + hi) ^ (ksw & 15))];
+        vaddr[ks] = (uint32_t)(uintptr_t)&lv[0][l32 * 16 + ((2 * ks + hi) ^ (l32 & 15))];
+    }
     issue_tile(0, 0);
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
@@ -245,7 +273,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
 #pragma unroll
                         for (int ks = 0; ks < 8; ++ks) s[mb] = mfma32x32x16(kfrag(mb, ks), qf[ks], s[mb]);
                     }
-            } else {
+            } else if constexpr (PAGED) {
 #pragma unroll
             for (int ks = 0; ks < 8; ++ks) {
                 const bf16x8 k0 = kfrag(0, ks), k1 = kfrag(1, ks), k2 = kfrag(2, ks), k3 = kfrag(3, ks);
@@ -254,6 +282,24 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 s[2] = mfma32x32x16(k2, qf[ks], s[2]);
                 s[3] = mfma32x32x16(k3, qf[ks], s[3]);
             }
+            } else {
+                u32x4 kf[3][4];
+                auto rd = [&](int ks, u32x4 (&f)[4]) __attribute__((always_inline)) {
+                    f[0] = ds_read16<stg * 32768 + 0>(kaddr[ks]);
+                    f[1] = ds_read16<stg * 32768 + 8192>(kaddr[ks]);
+                    f[2] = ds_read16<stg * 32768 + 16384>(kaddr[ks]);
+                    f[3] = ds_read16<stg * 32768 + 24576>(kaddr[ks]);
+                };
+                rd(0, kf[0]);
+                rd(1, kf[1]);
+#pragma unroll
+                for (int ks = 0; ks < 8; ++ks) {
+                    if (ks < 7) lgkm_wait<4>(kf[ks % 3]);
+                    else lgkm_wait<0>(kf[ks % 3]);
+                    if (ks + 2 < 8) rd(ks + 2, kf[(ks + 2) % 3]);
+#pragma unroll
+                    for (int mb = 0; mb < 4; ++mb) s[mb] = mfma32x32x16(as_bf16x8(kf[ks % 3][mb]), qf[ks], s[mb]);
+                }
             }
             // The next tile goes into the other buffer (read last before the previous barrier)
             // after the K fragment reads of this one, not in the same burst (1-2 % faster).
@@ -305,6 +351,7 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                     pb[mb][p] = as_bf16x8(w);
                 }
             // ---- O^T += V^T P^T: 32 MFMAs over 8 chunks of 16 positions -------------------
+            if constexpr (kDiag || PAGED) {
 #pragma unroll
             for (int c = 0; c < 8; ++c) {
                 const int mb = c >> 1, p = c & 1;
@@ -314,6 +361,25 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                     const int d = 32 * db + l32;
                     const bf16x8 vf = as_bf16x8(lv[stg][d * 16 + ((2 * c + hi) ^ (d & 15))]);
                     o[db] = mfma32x32x16(vf, pb[mb][p], o[db]);
+                }
+            }
+            } else {
+                u32x4 vf[3][4];
+                auto rd = [&](int c, u32x4 (&f)[4]) __attribute__((always_inline)) {
+                    f[0] = ds_read16<stg * 32768 + 0>(vaddr[c]);
+                    f[1] = ds_read16<stg * 32768 + 8192>(vaddr[c]);
+                    f[2] = ds_read16<stg * 32768 + 16384>(vaddr[c]);
+                    f[3] = ds_read16<stg * 32768 + 24576>(vaddr[c]);
+                };
+                rd(0, vf[0]);
+                rd(1, vf[1]);
+#pragma unroll
+                for (int c = 0; c < 8; ++c) {
+                    if (c < 7) lgkm_wait<4>(vf[c % 3]);
+                    else lgkm_wait<0>(vf[c % 3]);
+                    if (c + 2 < 8) rd(c + 2, vf[(c + 2) % 3]);
+#pragma unroll
+                    for (int db = 0; db < 4; ++db) o[db] = mfma32x32x16(as_bf16x8(vf[c % 3][db]), pb[c >> 1][c & 1], o[db]);
                 }
             }
         };

@@ -110,39 +110,44 @@ __global__ __launch_bounds__(256) void rope_scatter_kernel(const float* __restri
 __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__ A, WRows W, int M,
                                                        int N, int K, float* __restrict__ out,
                                                        const float* __restrict__ xres) {
-    __shared__ float As[16][68], Ws[16][68];
+    // 32 x 32 output tile (2 x 2 per thread), 64-wide K steps with all of a step's loads in
+    // flight at once: the fp32 models' GEMMs are small, so parallelism and latency matter.
+    __shared__ float As[64][36], Ws[64][36];
     const int tid = threadIdx.x, tx = tid & 15, ty = tid >> 4;
-    const int m0 = blockIdx.y * 64, n0 = blockIdx.x * 64;
-    float acc[4][4] = {};
-    for (int k0 = 0; k0 < K; k0 += 16) {
+    const int m0 = blockIdx.y * 32, n0 = blockIdx.x * 32;
+    float acc[2][2] = {};
+    for (int k0 = 0; k0 < K; k0 += 64) {
+        float av_[8], wv_[8];
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-            const int id = tid + 256 * i, row = id >> 4, kk = id & 15;
+        for (int i = 0; i < 8; ++i) {
+            const int id = tid + 256 * i, row = id >> 6, kk = id & 63;
             const int m = m0 + row, n = n0 + row, k = k0 + kk;
-            As[kk][row] = (m < M && k < K) ? A[(size_t)m * K + k] : 0.f;
-            Ws[kk][row] = (n < N && k < K) ? ((const float*)w_row_any(W, n, K, 4))[k] : 0.f;
+            av_[i] = (m < M && k < K) ? A[(size_t)m * K + k] : 0.f;
+            wv_[i] = (n < N && k < K) ? ((const float*)w_row_any(W, n, K, 4))[k] : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+            const int id = tid + 256 * i, row = id >> 6, kk = id & 63;
+            As[kk][row] = av_[i];
+            Ws[kk][row] = wv_[i];
         }
         __syncthreads();
-#pragma unroll
-        for (int kk = 0; kk < 16; ++kk) {
-            float av[4], bv[4];
-#pragma unroll
-            for (int i = 0; i < 4; ++i) {
-                av[i] = As[kk][ty * 4 + i];
-                bv[i] = Ws[kk][tx * 4 + i];
-            }
-#pragma unroll
-            for (int i = 0; i < 4; ++i)
-#pragma unroll
-                for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(av[i], bv[j], acc[i][j]);
+#pragma unroll 16
+        for (int kk = 0; kk < 64; ++kk) {
+            const float a0 = As[kk][ty * 2], a1 = As[kk][ty * 2 + 1];
+            const float b0 = Ws[kk][tx * 2], b1 = Ws[kk][tx * 2 + 1];
+            acc[0][0] = fmaf(a0, b0, acc[0][0]);
+            acc[0][1] = fmaf(a0, b1, acc[0][1]);
+            acc[1][0] = fmaf(a1, b0, acc[1][0]);
+            acc[1][1] = fmaf(a1, b1, acc[1][1]);
         }
         __syncthreads();
     }
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const int m = m0 + ty * 4 + i, n = n0 + tx * 4 + j;
+        for (int j = 0; j < 2; ++j) {
+            const int m = m0 + ty * 2 + i, n = n0 + tx * 2 + j;
             if (m < M && n < N) {
                 const size_t off = (size_t)m * N + n;
                 out[off] = xres ? xres[off] + acc[i][j] : acc[i][j];
@@ -150,16 +155,21 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(const float* __restrict__
         }
 }
 
+// One wave per (row, query head): the keys [0, pos] go through in chunks of 64, lane j
+// scoring key t0 + j (a D-long dot product from its K row); the chunk's maximum and sum are
+// wave reductions (online softmax in fp32), and lane j accumulates output dimensions j and
+// j + 64 over the chunk's keys, each key's weight broadcast from its lane.
 template <int D>
-__global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ q,
-                                                      const float* __restrict__ kc,
-                                                      const float* __restrict__ vc,
-                                                      const int32_t* __restrict__ lens,
-                                                      float* __restrict__ o, int rows, int S, int a,
-                                                      int g, int cap) {
-    const int idx = blockIdx.x * blockDim.x + threadIdx.x;
-    if (idx >= rows * a) return;
-    const int r = idx / a, h = idx - r * a, kvh = h / (a / g);
+__global__ __launch_bounds__(256) void attn_f32_kernel(const float* __restrict__ q,
+                                                       const float* __restrict__ kc,
+                                                       const float* __restrict__ vc,
+                                                       const int32_t* __restrict__ lens,
+                                                       float* __restrict__ o, int rows, int S, int a,
+                                                       int g, int cap) {
+    constexpr int DPL = (D + 63) / 64;   // output dimensions per lane
+    const int wid = (blockIdx.x * blockDim.x + threadIdx.x) >> 6, lane = threadIdx.x & 63;
+    if (wid >= rows * a) return;         // wave-uniform
+    const int r = wid / a, h = wid - r * a, kvh = h / (a / g);
     int b, pos;
     if (lens) {
         b = r;
@@ -169,30 +179,47 @@ __global__ __launch_bounds__(64) void attn_f32_kernel(const float* __restrict__ 
         pos = r - b * S;
     }
     const float scale = 1.0f / sqrtf((float)D);
-    float qv[D], acc[D];
+    float qv[D];
 #pragma unroll
-    for (int i = 0; i < D; ++i) {
-        qv[i] = q[((size_t)r * a + h) * D + i];
-        acc[i] = 0.f;
-    }
+    for (int i = 0; i < D; ++i) qv[i] = q[((size_t)r * a + h) * D + i];
     const float* kb = kc + ((size_t)b * g + kvh) * cap * D;
     const float* vb = vc + ((size_t)b * g + kvh) * D * cap;
+    float acc[DPL];
+#pragma unroll
+    for (int k = 0; k < DPL; ++k) acc[k] = 0.f;
     float m = -INFINITY, l = 0.f;
-    for (int t = 0; t <= pos; ++t) {
-        float s = 0.f;
+    for (int t0 = 0; t0 <= pos; t0 += 64) {
+        const int t = t0 + lane;
+        float sc = -INFINITY;
+        if (t <= pos) {
+            float d = 0.f;
 #pragma unroll
-        for (int i = 0; i < D; ++i) s = fmaf(qv[i], kb[(size_t)t * D + i], s);
-        s *= scale;
-        const float m_new = fmaxf(m, s);
-        const float alpha = expf(m - m_new), p = expf(s - m_new);
-        l = l * alpha + p;
+            for (int i = 0; i < D; ++i) d = fmaf(qv[i], kb[(size_t)t * D + i], d);
+            sc = d * scale;
+        }
+        const float m_new = fmaxf(m, wave_max(sc));      // finite: key t0 is always visible
+        const float alpha = expf(m - m_new);
+        const float p = t <= pos ? expf(sc - m_new) : 0.f;
+        l = l * alpha + wave_sum(p);
 #pragma unroll
-        for (int i = 0; i < D; ++i) acc[i] = acc[i] * alpha + p * vb[(size_t)i * cap + t];
+        for (int k = 0; k < DPL; ++k) acc[k] *= alpha;
+        const int nk = min(64, pos + 1 - t0);
+        for (int j = 0; j < nk; ++j) {
+            const float pj = __shfl(p, j);
+#pragma unroll
+            for (int k = 0; k < DPL; ++k) {
+                const int d = lane + 64 * k;
+                if (d < D) acc[k] = fmaf(pj, vb[(size_t)d * cap + t0 + j], acc[k]);
+            }
+        }
         m = m_new;
     }
     const float inv = 1.0f / l;
 #pragma unroll
-    for (int i = 0; i < D; ++i) o[((size_t)r * a + h) * D + i] = acc[i] * inv;
+    for (int k = 0; k < DPL; ++k) {
+        const int d = lane + 64 * k;
+        if (d < D) o[((size_t)r * a + h) * D + d] = acc[k] * inv;
+    }
 }
 
 }  // namespace
@@ -222,15 +249,15 @@ hipError_t rope_scatter(const float* proj, int nsplit, size_t split_stride, int 
 
 hipError_t gemm_f32(const float* a, const WRows& w, int M, int N, int K, float* out,
                     const float* x_res, hipStream_t st) {
-    dim3 grid((N + 63) / 64, (M + 63) / 64);
+    dim3 grid((N + 31) / 32, (M + 31) / 32);
     hipLaunchKernelGGL(gemm_f32_kernel, grid, dim3(256), 0, st, a, w, M, N, K, out, x_res);
     return hipGetLastError();
 }
 
 hipError_t attn_f32(const float* q, const float* kc, const float* vc, const int32_t* lens, float* o,
                     int rows, int S, int a, int g, int d, int cap, hipStream_t st) {
-    const int n = rows * a;
-    dim3 grid((n + 63) / 64), block(64);
+    const int n = rows * a;                  // one wave each, four waves per block
+    dim3 grid((n + 3) / 4), block(256);
     switch (d) {
         case 16: hipLaunchKernelGGL(attn_f32_kernel<16>, grid, block, 0, st, q, kc, vc, lens, o, rows, S, a, g, cap); break;
         case 32: hipLaunchKernelGGL(attn_f32_kernel<32>, grid, block, 0, st, q, kc, vc, lens, o, rows, S, a, g, cap); break;
