@@ -228,7 +228,164 @@ __global__ __launch_bounds__(256) void decode_qkv_epi_kernel(const float* __rest
     }
 }
 
+// ---------------------------------------------------------------------------
+// Small batches (M <= 16): full K per workgroup, epilogue fused.  Workgroup j owns 16
+// output columns; wave w multiplies the K slice [512 w, 512 w + 512) in 16 steps of 32
+// (v_mfma_f32_16x16x32_bf16, A = X rows read from global memory, B = W^T), exactly as a
+// workgroup of gemm_decode_kernel does for one slice, and the waves' 16 x 16 partial tiles
+// are added in LDS in slice order, so the sums equal the split path's bit for bit.  The
+// sum goes straight to the epilogue (no partial planes, no second kernel): RoPE at the
+// sequence's position and Q / K row / V^T column (projections), or the residual add
+// (output projection).  In the rotary region a workgroup takes columns 8 s .. 8 s + 7 of a
+// head's first half and the same of its second half, so both members of every rotary pair
+// are in one workgroup; elsewhere 16 consecutive columns.
+// ---------------------------------------------------------------------------
+struct FusedQkv {
+    uint16_t* q;
+    uint16_t* kc;
+    uint16_t* vc;
+    const int32_t* lens;
+    int a, g, cap, producer;
+    double base;
+    Pages pages;
+};
+struct FusedResid {
+    const void* xres;
+    int xres_f32;
+    uint16_t* y;
+    float* yf;
+};
+
+__device__ __forceinline__ const uint16_t* w_row3(const WRows& w, int n, int K) {
+    if (n < w.rows[0]) return (const uint16_t*)w.p[0] + (size_t)n * K;
+    n -= w.rows[0];
+    if (n < w.rows[1]) return (const uint16_t*)w.p[1] + (size_t)n * K;
+    n -= w.rows[1];
+    return (const uint16_t*)w.p[2] + (size_t)n * K;
+}
+
+template <int MODE>   // 0: projections with RoPE + cache append, 1: output projection + residual
+__global__ __launch_bounds__(1024) void gemm_decode_fused_kernel(const uint16_t* __restrict__ X, WRows W, int M,
+                                                                 int N, int K, FusedQkv fq, FusedResid fr) {
+    constexpr int D = 128, HALF = 64;
+    __shared__ float red[16][16 * 16];   // [wave][row * 16 + column]
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    const int col = lane & 15, kg = lane >> 4;
+    const int j = blockIdx.x;
+    const int nrot = MODE == 0 ? (fq.a + (fq.producer ? fq.g : 0)) * D : 0;   // rotary columns
+    const bool rot = 16 * j < nrot;
+    const int n = rot ? (j >> 3) * D + (col < 8 ? 0 : HALF) + (j & 7) * 8 + (col & 7) : 16 * j + col;
+    const int k0 = 512 * wave;
+    const uint16_t* wr = w_row3(W, n, K) + k0 + 8 * kg;
+    const uint16_t* xr = X + (size_t)min(col, M - 1) * K + k0 + 8 * kg;
+    u32x4 wf[16], xf[16];
+#pragma unroll
+    for (int s = 0; s < 16; ++s) {
+        wf[s] = *(const u32x4*)(wr + 32 * s);
+        xf[s] = *(const u32x4*)(xr + 32 * s);
+    }
+    f32x4 acc = f32x4{};
+#pragma unroll
+    for (int s = 0; s < 16; ++s) acc = mfma16x16x32(as_bf16x8(xf[s]), as_bf16x8(wf[s]), acc);
+    // Lane (col, kg) holds rows 4 kg + i of its column.
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][(4 * kg + i) * 16 + col] = acc[i];
+    __syncthreads();
+    auto sum = [&](int row, int c) {
+        float v = red[0][row * 16 + c];
+        for (int w = 1; w < nw; ++w) v += red[w][row * 16 + c];
+        return v;
+    };
+    // Epilogue items (16 rows x 16 columns, or 16 rows x 8 rotary pairs) go over the
+    // workgroup's threads (one wave when K = 512).
+    if constexpr (MODE == 1) {
+        for (int t = threadIdx.x; t < 16 * M; t += blockDim.x) {
+            const int row = t >> 4, c = t & 15;
+            const size_t off = (size_t)row * N + 16 * j + c;
+            const float xv = fr.xres_f32 ? ((const float*)fr.xres)[off]
+                                         : __uint_as_float((uint32_t)((const uint16_t*)fr.xres)[off] << 16);
+            const float r = xv + sum(row, c);
+            fr.y[off] = f2bf(r);
+            if (fr.yf) fr.yf[off] = r;
+        }
+    } else {
+        // Rows (in units of D elements) of head 0's block holding pos and the stride between
+        // heads' blocks: the slot of sequence b, or page pos / 64 of the head-major pools.
+        auto place = [&](int b, int pos, size_t& kv0, size_t& hstride, int& vld, int& prow) {
+            if (fq.pages.pt) {
+                kv0 = (size_t)page_at(fq.pages, b, pos / kPage) * kPage;
+                hstride = (size_t)fq.pages.n * kPage;
+                vld = kPage;
+                prow = pos % kPage;
+            } else {
+                kv0 = (size_t)b * fq.g * fq.cap;
+                hstride = fq.cap;
+                vld = fq.cap;
+                prow = pos;
+            }
+        };
+        if (rot) {
+            for (int t = threadIdx.x; t < 8 * M; t += blockDim.x) {
+                const int row = t >> 3, c = t & 7;
+                const int h = j >> 3, i = (j & 7) * 8 + c;
+                const int pos = max(0, min(fq.lens[row], fq.cap - 1));
+                const double theta = pow(fq.base, -2.0 * i / D);
+                double sd, cd;
+                sincos((double)pos * theta, &sd, &cd);
+                const float cs = (float)cd, sn = (float)sd;
+                const float x1 = sum(row, c), x2 = sum(row, c + 8);
+                const float o1 = x1 * cs - x2 * sn, o2 = x2 * cs + x1 * sn;
+                if (h < fq.a) {
+                    fq.q[(size_t)row * fq.a * D + h * D + i] = f2bf(o1);
+                    fq.q[(size_t)row * fq.a * D + h * D + i + HALF] = f2bf(o2);
+                } else {
+                    size_t kv0, hstride;
+                    int vld, prow;
+                    place(row, pos, kv0, hstride, vld, prow);
+                    const size_t kb = (kv0 + (size_t)(h - fq.a) * hstride + prow) * D;
+                    fq.kc[kb + i] = f2bf(o1);
+                    fq.kc[kb + i + HALF] = f2bf(o2);
+                }
+            }
+        } else {
+            for (int t = threadIdx.x; t < 16 * M; t += blockDim.x) {
+                const int row = t >> 4, c = t & 15;
+                const int pos = max(0, min(fq.lens[row], fq.cap - 1));
+                const int e = 16 * j - nrot + c, h = e / D, d = e - h * D;
+                size_t kv0, hstride;
+                int vld, prow;
+                place(row, pos, kv0, hstride, vld, prow);
+                fq.vc[(kv0 + (size_t)h * hstride) * D + (size_t)d * vld + prow] = f2bf(sum(row, c));
+            }
+        }
+    }
+}
+
 }  // namespace
+
+bool decode_fused_ok(int M, int N, int K) {
+    return M >= 1 && M <= 16 && N % 16 == 0 && K % 512 == 0 && K >= 512 && K <= 16 * 512;
+}
+
+hipError_t gemm_decode_qkv_fused_bf16(const uint16_t* x, const WRows& w, int B, int N, int K, const int32_t* lens,
+                                      int a, int g, int cap, double base, bool producer, uint16_t* q, uint16_t* kc,
+                                      uint16_t* vc, const Pages& pages, hipStream_t st) {
+    if (!decode_fused_ok(B, N, K) || N != (a + (producer ? 2 * g : 0)) * 128) return hipErrorInvalidValue;
+    if (pages.pt && (pages.n < 1 || pages.stride < 1 || cap != kPage * pages.stride)) return hipErrorInvalidValue;
+    FusedQkv fq{q, kc, vc, lens, a, g, cap, producer ? 1 : 0, base, pages};
+    hipLaunchKernelGGL(gemm_decode_fused_kernel<0>, dim3(N / 16), dim3(64 * (K / 512)), 0, st, x, w, B, N, K, fq,
+                       FusedResid{});
+    return hipGetLastError();
+}
+
+hipError_t gemm_decode_resid_fused_bf16(const uint16_t* x, const WRows& w, int M, int N, int K, const void* x_res,
+                                        bool x_f32, uint16_t* y, float* yf, hipStream_t st) {
+    if (!decode_fused_ok(M, N, K)) return hipErrorInvalidValue;
+    FusedResid fr{x_res, x_f32 ? 1 : 0, y, yf};
+    hipLaunchKernelGGL(gemm_decode_fused_kernel<1>, dim3(N / 16), dim3(64 * (K / 512)), 0, st, x, w, M, N, K,
+                       FusedQkv{}, fr);
+    return hipGetLastError();
+}
 
 int decode_gemm_splits(int K) {
     const int kc = decode_kc(K);

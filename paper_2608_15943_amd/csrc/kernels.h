@@ -146,6 +146,16 @@ hipError_t decode_resid_bf16(const float* part, int nsplit, int M, int N, const 
 hipError_t decode_qkv_epilogue_bf16(const float* part, int nsplit, int B, int N, const int32_t* lens, int a,
                                     int g, int cap, double base, bool producer, uint16_t* q, uint16_t* kc,
                                     uint16_t* vc, const Pages& pages, hipStream_t st);
+// Small batches (M <= 16, K % 512 == 0, K <= 8192): the same products with the whole K in
+// one workgroup per 16 columns and the epilogue fused (RoPE + Q / K / V^T writes as
+// decode_qkv_epilogue_bf16, or the residual as decode_resid_bf16); results equal the split
+// path's bit for bit.
+bool decode_fused_ok(int M, int N, int K);
+hipError_t gemm_decode_qkv_fused_bf16(const uint16_t* x, const WRows& w, int B, int N, int K, const int32_t* lens,
+                                      int a, int g, int cap, double base, bool producer, uint16_t* q, uint16_t* kc,
+                                      uint16_t* vc, const Pages& pages, hipStream_t st);
+hipError_t gemm_decode_resid_fused_bf16(const uint16_t* x, const WRows& w, int M, int N, int K, const void* x_res,
+                                        bool x_f32, uint16_t* y, float* yf, hipStream_t st);
 
 // Attention of one new query per sequence over positions [0, len_b], on a grid of
 // `waves` single-wave workgroups that split the (sequence, KV head, tile) list evenly.

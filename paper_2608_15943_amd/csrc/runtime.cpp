@@ -362,7 +362,18 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
     void* o = ws + w.o;
     int rc;
     const int nsplit = c->bf16() ? kvp::decode_gemm_splits(h) : 1;
-    if ((rc = timed(c, KVP_K_DEC_GEMM, st, [&] {
+    // Small batches: one kernel per projection with its epilogue fused (same sums, bit for bit).
+    const bool fused = c->bf16() && kvp::decode_fused_ok(B, N, h) && kvp::decode_fused_ok(B, h, nq);
+    if (fused) {
+        if ((rc = timed(c, KVP_K_DEC_GEMM, st, [&] {
+                 return check_hip(kvp::gemm_decode_qkv_fused_bf16((const uint16_t*)io.a, wr, B, N, h, lens, c->d.a,
+                                                                  c->d.g, kv.cap, c->d.rope_base, producer,
+                                                                  (uint16_t*)q, producer ? (uint16_t*)kv.k : nullptr,
+                                                                  producer ? (uint16_t*)kv.v : nullptr, kv.pages, st),
+                                  "decode projection GEMM (fused)");
+             })))
+            return rc;
+    } else if ((rc = timed(c, KVP_K_DEC_GEMM, st, [&] {
              return c->bf16()
                         ? check_hip(kvp::gemm_decode_bf16((const uint16_t*)io.a, wr, B, N, h, proj, st),
                                     "decode projection GEMM")
@@ -370,7 +381,7 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
                                     "decode projection GEMM (fp32)");
          })))
         return rc;
-    if ((rc = timed(c, KVP_K_DEC_ROPE, st, [&] {
+    if (!fused && (rc = timed(c, KVP_K_DEC_ROPE, st, [&] {
              return c->bf16()
                         ? check_hip(kvp::decode_qkv_epilogue_bf16(
                                         proj, nsplit, B, N, lens, c->d.a, c->d.g, kv.cap,
@@ -400,6 +411,12 @@ int run_decode_layer(kvp_ctx* c, int l, const LayerIO& io, const int32_t* lens,
                                   "decode combine");
              })))
             return rc;
+        if (fused)
+            return timed(c, KVP_K_DEC_OPROJ, st, [&] {
+                return check_hip(kvp::gemm_decode_resid_fused_bf16((const uint16_t*)o, wo, B, h, nq, io.res,
+                                                                   io.res_f32, (uint16_t*)io.y, io.yf, st),
+                                 "decode output projection (fused)");
+            });
         return timed(c, KVP_K_DEC_OPROJ, st, [&] {
             const int ns = kvp::decode_gemm_splits(nq);
             int r2 = check_hip(kvp::gemm_decode_bf16((const uint16_t*)o, wo, B, h, nq, proj, st),
