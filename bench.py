@@ -495,36 +495,21 @@ def mall_probe(sizes_mib=(32, 64, 128, 192, 256, 384, 512), trials: int = 5):
     return out
 
 
-def kernel_fracs(tflops: dict) -> dict:
-    """Every MFMA kernel's algorithmic TFLOP/s against the datasheet and the measured peak."""
+def kernel_fracs(tflops: dict, workload=None) -> dict:
+    """Every MFMA kernel's algorithmic TFLOP/s against the datasheet and the measured peak, with
+    the committed matrix-core counters of that kernel on that workload (mfma_counters_for)."""
     ach = ACHIEVABLE.get("mfma_bf16_tflops")
     return {k: {"tflops": v, "frac": round(v / PEAK_BF16_TFLOPS, 4),
-                "frac_achievable": round(v / ach, 4) if ach else None} for k, v in tflops.items()}
+                "frac_achievable": round(v / ach, 4) if ach else None,
+                "mfma_counters": mfma_counters_for(k, workload) if workload else None}
+            for k, v in tflops.items()}
 
 
-def roofline_entry(kernel, prof, per_unit, units_per_launch, peak, unit, bound, workload):
-    """Algorithmic work per launch (per-unit figure x units one launch processes) over the
-    kernel's average launch time, measured with HIP events on the launch stream."""
-    n, t = prof[kernel]
-    per_launch = per_unit * units_per_launch
-    achieved = per_launch / (t / n * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
-    ent = {"bound": bound, "kernel": kernel, "achieved": round(achieved, 2), "peak": peak,
-           "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel, workload),
-           "work_per_launch": per_launch, "avg_launch_ms": round(t / n, 5)}
-    # The same figure against what this device measurably delivers (achievable_peaks).
-    ach = ACHIEVABLE.get("mfma_bf16_tflops" if unit == "TFLOP/s" else "hbm_read_gbs")
-    if ach:
-        ent["peak_achievable"] = ach
-        ent["frac_achievable"] = round(achieved / ach, 4)
-    return ent
-
-
-def traffic_for(kernel, workload):
-    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE counter runs (scaled by
-    the factor a plain copy of known size gives) of this kernel on this workload, or None if
-    there is none or the kernel's sources differ from the ones the counters were taken on."""
+def _committed(name, kernel, workload):
+    """Entry kernel@workload of profiles/<name>, or None if there is none or the kernel's
+    sources differ from the ones the counters were taken on."""
     import hashlib
-    path = os.path.join(ROOT, "profiles", "traffic.json")
+    path = os.path.join(ROOT, "profiles", name)
     if not os.path.exists(path):
         return None
     with open(path) as f:
@@ -538,9 +523,46 @@ def traffic_for(kernel, workload):
             return None
         with open(src, "rb") as f:
             h.update(f.read())
-    if h.hexdigest() != ent["sources_sha1"]:
+    return ent if h.hexdigest() == ent["sources_sha1"] else None
+
+
+def mfma_counters_for(kernel, workload):
+    """The committed rocprofv3 matrix-core counters of this kernel on this workload
+    (profiles/mfma.json, profiles/prefill_mfma_counters.md): the share of cycles its matrix cores
+    were busy, the clock it ran at, and the datasheet fraction they imply (busy x clock / 2.4
+    GHz), which corroborates the event-timed frac.  None if the sources changed since."""
+    ent = _committed("mfma.json", kernel, workload)
+    if not ent:
         return None
-    return ent["bytes_per_launch"]
+    return {"mfma_busy": ent["mfma_busy"], "clock_ghz": ent["clock_ghz"],
+            "implied_frac": round(ent["mfma_busy"] * ent["clock_ghz"] / 2.4, 4),
+            "bf16_flop_counted_per_dispatch": ent["bf16_flop_counted"]}
+
+
+def roofline_entry(kernel, prof, per_unit, units_per_launch, peak, unit, bound, workload):
+    """Algorithmic work per launch (per-unit figure x units one launch processes) over the
+    kernel's average launch time, measured with HIP events on the launch stream."""
+    n, t = prof[kernel]
+    per_launch = per_unit * units_per_launch
+    achieved = per_launch / (t / n * 1e-3) / (1e12 if unit == "TFLOP/s" else 1e9)
+    ent = {"bound": bound, "kernel": kernel, "achieved": round(achieved, 2), "peak": peak,
+           "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic_for(kernel, workload),
+           **({"mfma_counters": mfma_counters_for(kernel, workload)} if bound == "mfma" else {}),
+           "work_per_launch": per_launch, "avg_launch_ms": round(t / n, 5)}
+    # The same figure against what this device measurably delivers (achievable_peaks).
+    ach = ACHIEVABLE.get("mfma_bf16_tflops" if unit == "TFLOP/s" else "hbm_read_gbs")
+    if ach:
+        ent["peak_achievable"] = ach
+        ent["frac_achievable"] = round(achieved / ach, 4)
+    return ent
+
+
+def traffic_for(kernel, workload):
+    """HBM bytes per launch from the committed FETCH_SIZE / WRITE_SIZE counter runs (scaled by
+    the factor a plain copy of known size gives) of this kernel on this workload, or None if
+    there is none or the kernel's sources differ from the ones the counters were taken on."""
+    ent = _committed("traffic.json", kernel, workload)
+    return ent["bytes_per_launch"] if ent else None
 
 
 def main():
@@ -642,7 +664,7 @@ def main():
                               for k in flops if k in prof},
         "finite": finite,
     }
-    result["per_kernel_roofline"] = kernel_fracs(result["per_kernel_tflops"])
+    result["per_kernel_roofline"] = kernel_fracs(result["per_kernel_tflops"], w.name)
 
     if not args.no_unshared:
         ident = list(range(w.L))
@@ -1046,7 +1068,7 @@ def bench_70b(steps: int, warmup: int, unshared: bool = False, cpu: bool = False
            "kernels": {k: {"launches": n, "avg_ms": round(t / n, 5)} for k, (n, t) in prof5.items()},
            "per_kernel_tflops": {k: round(fl5[k] * steps5 / prof5[k][1] / 1e9, 1)
                                  for k in fl5 if k in prof5}}
-    out["per_kernel_roofline"] = kernel_fracs(out["per_kernel_tflops"])
+    out["per_kernel_roofline"] = kernel_fracs(out["per_kernel_tflops"], w5.name)
     log(f"[bench] 70B stage {ms5:.3f} ms/step, {out['tflops']} TFLOP/s")
     if unshared:
         ident = list(range(w5.L))
