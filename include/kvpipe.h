@@ -17,9 +17,13 @@
  * - Every call returns an int status: KVP_OK (0) or a negative KVP_E_* code.
  *   No C++ exception crosses this boundary.  kvp_last_error() returns a
  *   thread-local message describing the last failure on the calling thread.
- * - The library allocates no device memory.  The caller owns weights,
- *   activations, KV caches and the workspace (its size comes from
- *   kvp_workspace_size).  Host-side plan state lives in an opaque kvp_ctx.
+ * - The library allocates no device memory at run time.  The caller owns
+ *   weights, activations, KV caches and the workspace (its size comes from
+ *   kvp_workspace_size; every compute call takes it as ws / ws_bytes, so that
+ *   the calls never allocate).  The one piece of device memory the library
+ *   holds is the file-scope array that kvp_decode_step_noalloc uses in place
+ *   of a workspace (64 MiB per GPU, loaded with the library).  Host-side plan
+ *   state lives in an opaque kvp_ctx.
  * - Device pointers are plain `void*` into device memory of the current HIP
  *   device.  Device work is enqueued asynchronously on the caller's stream
  *   (`stream` is a hipStream_t passed as void*, NULL = the null stream); the
@@ -37,7 +41,9 @@
  *     K slot             [B_max][g][kv_capacity][d_h]   post-RoPE keys
  *     V slot             [B_max][g][d_h][kv_capacity]   values, transposed so
  *                        that both attention contractions read contiguous
- *                        runs of the cache (see kvp_set_kv_slot).
+ *                        runs of the cache (see kvp_set_kv_slot): a deliberate
+ *                        departure from a row-major [B][g][kv_capacity][d_h]
+ *                        V cache.
  *     attention output   [B, S, a * d_h]      (concatenated heads)
  * - RoPE: rotate-half pairing (x_i, x_{i + d_h/2}), theta_i =
  *   rope_base^(-2i/d_h), absolute positions 0..S-1 in prefill and len_b in
