@@ -162,10 +162,44 @@ def test_decode_fp32_tiny():
     (1024, 8, 8, [0, 1], [2000], 2048),                       # MHA
     (512, 4, 1, [0, 0], [5000, 3, 4095], 5120),                # ragged, > 1 split
     (512, 4, 2, [0, 0, 2], [127, 0, 64, 1], 128),             # new token in the slot's last position
+    # 37 sequences: above the fused small-batch projections, so the split-K projection kernels
+    # run with a partial 16-row block (rows 32-36 of 48)
+    (512, 4, 2, [0, 0, 2], [(37 * i) % 301 for i in range(37)], 384),
 ])
 def test_decode_bf16(h, a, g, tau, lens, cap):
     w = small_workload(f"dec-h{h}-a{a}-g{g}", len(tau), h, a, g, tau)
     _decode_case(w, len(lens), lens, cap)
+
+
+def test_decode_fused_projections_equal_split_k():
+    """Batches of up to 16 sequences run each projection as one fused kernel, larger ones as
+    split-K partial sums plus epilogue kernels; both add the K slices in the same order, so a
+    sequence's outputs and appended K/V are the same bits whichever path its batch takes.
+    Sequence b's input and caches do not depend on the batch size: the first 16 sequences of
+    a 17-sequence call (split-K) must equal a 16-sequence call (fused) bit for bit."""
+    w = small_workload("dec-fused-vs-split", 3, 512, 4, 2, [0, 0, 2])
+    cap = 384
+    lens17 = [(53 * i + 11) % 300 for i in range(17)]
+    out = {}
+    for B in (16, 17):
+        lens = lens17[:B]
+        dm = build_device_model(w, B, 1, cap, fill_cache_npos=max(lens))
+        x = torch.empty((B, w.h), dtype=tdtype(w), device=DEV)
+        kd.fill_decode_x(w, x.data_ptr(), B)
+        y = torch.empty_like(x)
+        lens_t = torch.tensor(lens, dtype=torch.int32, device=DEV)
+        ws_t, n = workspace(dm, kb.KVP_PHASE_DECODE, B)
+        dm.model.kvp_decode_step(x.data_ptr(), lens_t.data_ptr(), max(lens), y.data_ptr(), B,
+                                 ws_t.data_ptr(), n, torch.cuda.current_stream().cuda_stream)
+        torch.cuda.synchronize()
+        kv = {p: (torch.stack([K[b, :, lens[b]] for b in range(16)]),
+                  torch.stack([V[b, :, :, lens[b]] for b in range(16)])) for p, (K, V) in dm.slots.items()}
+        out[B] = (y[:16].clone(), kv)
+        del dm, x, y, ws_t
+    assert torch.equal(out[16][0], out[17][0])
+    for p in out[16][1]:
+        assert torch.equal(out[16][1][p][0], out[17][1][p][0])
+        assert torch.equal(out[16][1][p][1], out[17][1][p][1])
 
 
 def test_identity_map_equals_unshared_run_of_same_weights():
