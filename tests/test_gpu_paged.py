@@ -70,6 +70,8 @@ def gather(pools, tab_t, b, npos):
     (512, 4, 1, [0, 0, 2], [0, 1, 63, 64, 200, 130], 4),     # r = 4, tile and page edges
     (512, 4, 2, [0, 0, 0], [300, 1000, 257], 17),            # r = 2, several splits, spare row
     (512, 4, 2, [0, 0, 2], [127, 0, 255], 4),                # new token in the row's last page
+    # 37 sequences: the split-K projections with their epilogue appending through the table
+    (512, 4, 2, [0, 0, 2], [(29 * i + 5) % 260 for i in range(37)], 5),
 ])
 def test_decode_paged_equals_slots(h, a, g, tau, lens, stride):
     w = small_workload(f"paged-dec-h{h}-a{a}-g{g}", len(tau), h, a, g, tau, seed=31)
