@@ -115,6 +115,7 @@ def _train_case(w, B, S, cap):
     (512, 4, 1, [0, 1, 1], 3, 130),          # r = 4, batch of 3, S just past a key block
     (256, 2, 1, [0, 0], 2, 1),               # S = 1
     (256, 2, 1, [0, 0, 2], 2, 256),          # 512 tokens: weight gradients on token-major copies
+    (1024, 8, 1, [0, 0], 1, 160),            # r = 8 (the 70B-shaped ratio), one consumer
 ])
 def test_backward_matches_oracle(h, a, g, tau, B, S):
     w = small_workload(f"bwd-h{h}-a{a}-g{g}", len(tau), h, a, g, tau, seed=21)
