@@ -165,6 +165,9 @@ def test_decode_fp32_tiny():
     # 37 sequences: above the fused small-batch projections, so the split-K projection kernels
     # run with a partial 16-row block (rows 32-36 of 48)
     (512, 4, 2, [0, 0, 2], [(37 * i) % 301 for i in range(37)], 384),
+    # d_model 8192 (K = 8192): fused projections with 16 waves per workgroup, and split-K
+    (8192, 64, 8, [0, 0], [5, 70, 130], 192),
+    (8192, 64, 8, [0, 0], [(41 * i + 3) % 180 for i in range(20)], 192),
 ])
 def test_decode_bf16(h, a, g, tau, lens, cap):
     w = small_workload(f"dec-h{h}-a{a}-g{g}", len(tau), h, a, g, tau)
