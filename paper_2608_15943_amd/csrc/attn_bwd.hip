@@ -29,6 +29,7 @@
 #include <math.h>
 
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -38,6 +39,41 @@ namespace kvp {
 namespace {
 
 constexpr int D = 128;
+
+// Transposed LDS reads placed by hand (see the dK, dV kernel): 8 bytes per lane at a per-lane
+// address plus an immediate offset; a wait names the fragment it completes as an in/out
+// operand, so the MFMA that reads it cannot be scheduled before it.
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+template <int OFF>
+__device__ __forceinline__ u32x2_t tr_read(uint32_t addr) {
+    u32x2_t v;
+    asm volatile("ds_read_b64_tr_b16 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+    return v;
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait2(u32x2_t& lo, u32x2_t& up) {
+    asm volatile("s_waitcnt lgkmcnt(%2)" : "+v"(lo), "+v"(up) : "i"(N));
+}
+template <int N, int I = 0, class F>
+__device__ __forceinline__ void static_for(F&& f) {
+    if constexpr (I < N) {
+        f(std::integral_constant<int, I>{});
+        static_for<N, I + 1>(f);
+    }
+}
+template <int OFF>
+__device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
+    u32x4 v;
+    asm volatile("ds_read_b128 %0, %1 offset:%2" : "=v"(v) : "v"(addr), "i"(OFF));
+    return v;
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait4(u32x4& a, u32x4& b, u32x2_t& c, u32x2_t& d) {
+    asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "i"(N));
+}
+__device__ __forceinline__ bf16x8 join_frag(u32x2_t lo, u32x2_t up) {
+    return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], up[0], up[1]});
+}
 
 typedef __attribute__((address_space(1))) void gvoid_t;
 typedef __attribute__((address_space(3))) void lvoid_t;
@@ -276,24 +312,66 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
         dv[i] = f32x16{};
     }
     const int rsw = swap_b23(l32);
+    // The transposed-read lane offsets of tr_frag<KV_BQ, false> (row r0 = 0, column block 0):
+    // the rest of a fragment's address is an immediate.
+    const int tr_row = 8 * (lane >> 5) + ((lane & 15) >> 2), tr_col = 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+    const int tr_lo = sub_off<KV_BQ>(tr_row, tr_col), tr_up = sub_off<KV_BQ>(tr_row + 4, tr_col);
+    // Row chunks of row8<KV_BQ>(tile, rsw, 16 ks + 8 hi) for even and odd ks (block 0, rows
+    // 0..31), and the V^T fragment of tr_frag<D, false>(lvt, 16 ks, 32 wave) at ks = 0.
+    const int rc0 = sub_off<KV_BQ>(rsw, 8 * hi), rc1 = sub_off<KV_BQ>(rsw, 16 + 8 * hi);
+    const uint32_t av_lo = (uint32_t)(uintptr_t)((const char*)lvt + wave * (D * 64) + sub_off<D>(tr_row, tr_col)),
+                   av_up = (uint32_t)(uintptr_t)((const char*)lvt + wave * (D * 64) + sub_off<D>(tr_row + 4, tr_col));
 
     if (n_it > 0) issue(0, 0);
-    for (int it = 0; it < n_it; ++it) {
-        const int stg = it & 1;
+    // Per-lane LDS addresses in stage 0 (stage 1 is a constant offset further: the loop below
+    // takes the stage as a compile-time constant): the two transposed reads of a dO / Q
+    // fragment (row block 0, column block 0), and the lane's Q / dO row chunk (row rsw,
+    // chunk 2 (ks & 1) + hi).  The k step's block, the half's rows and the stage are immediates.
+    const uint32_t o_lo = (uint32_t)(uintptr_t)((const char*)ldo_[0] + tr_lo),
+                   o_up = (uint32_t)(uintptr_t)((const char*)ldo_[0] + tr_up),
+                   q_lo = (uint32_t)(uintptr_t)((const char*)lq[0] + tr_lo),
+                   q_up = (uint32_t)(uintptr_t)((const char*)lq[0] + tr_up);
+    const uint32_t aq0 = (uint32_t)(uintptr_t)((const char*)lq[0] + rc0),
+                   aq1 = (uint32_t)(uintptr_t)((const char*)lq[0] + rc1),
+                   ao0 = (uint32_t)(uintptr_t)((const char*)ldo_[0] + rc0),
+                   ao1 = (uint32_t)(uintptr_t)((const char*)ldo_[0] + rc1);
+    constexpr int kStage = KV_BQ * 16 * 16;   // bytes of one stage of lq / ldo_
+    auto iteration = [&](int it, auto stg_t) __attribute__((always_inline)) {
+        constexpr int stg = decltype(stg_t)::value;
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();                          // tile it landed; tile it - 1 fully read
         if (it + 1 < n_it) issue(it + 1, stg ^ 1);
         const int qb0 = (qb_lo + it % nq_h) * KV_BQ;
-#pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
-            if (qb0 + 32 * rb + 31 < k0w) continue;   // every query of the half precedes the wave's keys
+        auto half = [&](auto rb_t) __attribute__((always_inline)) {
+            constexpr int RB = decltype(rb_t)::value;
+            const int rb = RB;
+            if (qb0 + 32 * rb + 31 < k0w) return;   // every query of the half precedes the wave's keys
             f32x16 s = f32x16{}, dp = f32x16{};
-            const int row = 32 * rb + rsw;
-#pragma unroll
-            for (int ks = 0; ks < 8; ++ks) {
-                s = mfma32x32x16(row8<KV_BQ>(lq[stg], row, 16 * ks + 8 * hi), kf[ks], s);
-                dp = mfma32x32x16(row8<KV_BQ>(ldo_[stg], row, 16 * ks + 8 * hi),
-                                  tr_frag<D, false>(lvt, 16 * ks, 32 * wave, lane), dp);
+            // S = Q K^T and dP = dO V^T over 8 k steps; step ks reads a Q row chunk, a dO row
+            // chunk and a V^T fragment (two transposed reads), one step ahead of its products.
+            {
+                u32x4 fq[2], fo[2];
+                u32x2_t fvl[2], fvu[2];
+                auto rd = [&](auto ks_t) __attribute__((always_inline)) {
+                    constexpr int ks = decltype(ks_t)::value;
+                    constexpr int roff = stg * kStage + (ks >> 1) * (KV_BQ * 64) + 2048 * RB, voff = ks * 1024;
+                    fq[ks % 2] = ds_read16<roff>(ks & 1 ? aq1 : aq0);
+                    fo[ks % 2] = ds_read16<roff>(ks & 1 ? ao1 : ao0);
+                    fvl[ks % 2] = tr_read<voff>(av_lo);
+                    fvu[ks % 2] = tr_read<voff>(av_up);
+                };
+                rd(std::integral_constant<int, 0>{});
+                static_for<8>([&](auto ks_t) __attribute__((always_inline)) {
+                    constexpr int ks = decltype(ks_t)::value;
+                    if constexpr (ks + 1 < 8) {
+                        rd(std::integral_constant<int, ks + 1>{});
+                        lgkm_wait4<4>(fq[ks % 2], fo[ks % 2], fvl[ks % 2], fvu[ks % 2]);
+                    } else {
+                        lgkm_wait4<0>(fq[ks % 2], fo[ks % 2], fvl[ks % 2], fvu[ks % 2]);
+                    }
+                    s = mfma32x32x16(as_bf16x8(fq[ks % 2]), kf[ks], s);
+                    dp = mfma32x32x16(as_bf16x8(fo[ks % 2]), join_frag(fvl[ks % 2], fvu[ks % 2]), dp);
+                });
             }
             // Register i holds query qb0 + 32 rb + 16 (i / 8) + 8 hi + i % 8.
             bf16x8 pa[2], da[2];
@@ -318,14 +396,40 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
                 pa[h] = pack8(pe);
                 da[h] = pack8(de);
             }
-#pragma unroll
-            for (int h = 0; h < 2; ++h)
-#pragma unroll
-                for (int nb = 0; nb < 4; ++nb) {
-                    dv[nb] = mfma32x32x16(pa[h], tr_frag<KV_BQ, false>(ldo_[stg], 32 * rb + 16 * h, 32 * nb, lane), dv[nb]);
-                    dk[nb] = mfma32x32x16(da[h], tr_frag<KV_BQ, false>(lq[stg], 32 * rb + 16 * h, 32 * nb, lane), dk[nb]);
-                }
-        }
+            // dV += P^T dO, dK += dS^T Q: 16 products, product i = (h, nb, dV or dK) =
+            // (i / 8, i / 2 % 4, i % 2), each B fragment two transposed reads.  The reads go two
+            // products ahead through three rotating fragments (the compiled order waited for
+            // each fragment right before its product).
+            {
+                u32x2_t flo[3], fup[3];
+                auto issue = [&](auto i_t) __attribute__((always_inline)) {
+                    constexpr int i = decltype(i_t)::value;
+                    constexpr int h = i / 8, nb = (i / 2) % 4;
+                    constexpr int off = stg * kStage + nb * (KV_BQ * 64) + (32 * RB + 16 * h) * 64;
+                    const uint32_t a_lo = (i % 2) ? q_lo : o_lo, a_up = (i % 2) ? q_up : o_up;
+                    flo[i % 3] = tr_read<off>(a_lo);
+                    fup[i % 3] = tr_read<off>(a_up);
+                };
+                issue(std::integral_constant<int, 0>{});
+                issue(std::integral_constant<int, 1>{});
+                static_for<16>([&](auto i_t) __attribute__((always_inline)) {
+                    constexpr int i = decltype(i_t)::value;
+                    constexpr int h = i / 8, nb = (i / 2) % 4;
+                    if constexpr (i + 1 < 16) lgkm_wait2<2>(flo[i % 3], fup[i % 3]);
+                    else lgkm_wait2<0>(flo[i % 3], fup[i % 3]);
+                    if constexpr (i + 2 < 16) issue(std::integral_constant<int, i + 2>{});
+                    const bf16x8 f = join_frag(flo[i % 3], fup[i % 3]);
+                    if constexpr (i % 2 == 0) dv[nb] = mfma32x32x16(pa[h], f, dv[nb]);
+                    else dk[nb] = mfma32x32x16(da[h], f, dk[nb]);
+                });
+            }
+        };
+        half(std::integral_constant<int, 0>{});
+        half(std::integral_constant<int, 1>{});
+    };
+    for (int it = 0; it < n_it; it += 2) {
+        iteration(it, std::integral_constant<int, 0>{});
+        if (it + 1 < n_it) iteration(it + 1, std::integral_constant<int, 1>{});
     }
 
     // Epilogue: lane column d = 32 nb + l32; register e of block nb holds key
