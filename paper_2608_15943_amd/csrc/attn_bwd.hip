@@ -40,9 +40,11 @@ namespace {
 
 constexpr int D = 128;
 
-// Transposed LDS reads placed by hand (see the dK, dV kernel): 8 bytes per lane at a per-lane
-// address plus an immediate offset; a wait names the fragment it completes as an in/out
-// operand, so the MFMA that reads it cannot be scheduled before it.
+// LDS reads placed by hand (the dK, dV and the dQ kernels): a transposed read moves 8 bytes
+// per lane, a row read 16, each from a per-lane address plus an immediate offset; a wait
+// names the fragments it completes as in/out operands, so the MFMA that reads one cannot be
+// scheduled before it.  LDS reads return in order, so a wait for at most N outstanding
+// operations completes every read but the last N issued.
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 template <int OFF>
 __device__ __forceinline__ u32x2_t tr_read(uint32_t addr) {
@@ -70,6 +72,10 @@ __device__ __forceinline__ u32x4 ds_read16(uint32_t addr) {
 template <int N>
 __device__ __forceinline__ void lgkm_wait4(u32x4& a, u32x4& b, u32x2_t& c, u32x2_t& d) {
     asm volatile("s_waitcnt lgkmcnt(%4)" : "+v"(a), "+v"(b), "+v"(c), "+v"(d) : "i"(N));
+}
+template <int N>
+__device__ __forceinline__ void lgkm_wait3(u32x4& a, u32x2_t& b, u32x2_t& c) {
+    asm volatile("s_waitcnt lgkmcnt(%3)" : "+v"(a), "+v"(b), "+v"(c) : "i"(N));
 }
 __device__ __forceinline__ bf16x8 join_frag(u32x2_t lo, u32x2_t up) {
     return __builtin_bit_cast(bf16x8, u32x4{lo[0], lo[1], up[0], up[1]});
@@ -559,29 +565,59 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
     for (int i = 0; i < 4; ++i) dq[i] = f32x16{};
     const int rsw = swap_b23(l32);
 
-    issue(0, 0);
-    for (int t = 0; t < ntiles; ++t) {
-        const int stg = t & 1;
+    // Per-lane LDS addresses in stage 0 (stage 1 is a constant offset further: the loop below
+    // takes the stage as a compile-time constant).  K row chunk of row8<Q_BKV>(lk, rsw,
+    // 16 ks + 8 hi) for even and odd ks; the two transposed reads of tr_frag<D, true>(lvt, 0, 0)
+    // and of tr_frag<Q_BKV, false>(lk, 0, 0).  Row blocks, column blocks, k steps and the
+    // stage are immediates.
+    const int G = lane >> 4, a4 = lane & 3;
+    const int tr_row = 8 * (G >> 1) + ((lane & 15) >> 2);
+    const int tr_col = 16 * (G & 1) + 4 * a4, trp_col = 16 * (G & 1) + 4 * (((a4 & 1) << 1) | (a4 >> 1));
+    const uint32_t k_base = (uint32_t)(uintptr_t)lk[0], v_base = (uint32_t)(uintptr_t)lvt[0];
+    const uint32_t ak0 = k_base + sub_off<Q_BKV>(rsw, 8 * hi), ak1 = k_base + sub_off<Q_BKV>(rsw, 16 + 8 * hi);
+    const uint32_t pv_lo = v_base + sub_off<D>(tr_row, trp_col), pv_up = v_base + sub_off<D>(tr_row + 4, trp_col);
+    const uint32_t tk_lo = k_base + sub_off<Q_BKV>(tr_row, tr_col), tk_up = k_base + sub_off<Q_BKV>(tr_row + 4, tr_col);
+    constexpr int kStage = Q_BKV * 16 * 16;   // bytes of one stage of lk (and of lvt: D == Q_BKV)
+    static_assert(D == Q_BKV, "one stage size for lk and lvt");
+
+    auto tile = [&](int t, auto stg_t) __attribute__((always_inline)) {
+        constexpr int stg = decltype(stg_t)::value;
         asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
         __syncthreads();
         if (t + 1 < ntiles) issue(t + 1, stg ^ 1);
         const int t0 = t * Q_BKV;
-        if (q0w >= A.S) continue;
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-            const int k0 = 64 * hf;                         // first key of the half in the tile
-            if (t0 + k0 > q0w + 31) continue;              // no key of the half is visible
+        if (q0w >= A.S) return;
+        auto half = [&](auto hf_t) __attribute__((always_inline)) {
+            constexpr int HF = decltype(hf_t)::value;
+            constexpr int k0 = 64 * HF;                     // first key of the half in the tile
+            if (t0 + k0 > q0w + 31) return;                // no key of the half is visible
             f32x16 s[2], dp[2];
-#pragma unroll
-            for (int mb = 0; mb < 2; ++mb) {
-                s[mb] = f32x16{};
-                dp[mb] = f32x16{};
-                const int row = k0 + 32 * mb + rsw;
-#pragma unroll
-                for (int ks = 0; ks < 8; ++ks) {
-                    s[mb] = mfma32x32x16(row8<Q_BKV>(lk[stg], row, 16 * ks + 8 * hi), qf[ks], s[mb]);
-                    dp[mb] = mfma32x32x16(tr_frag<D, true>(lvt[stg], 16 * ks, k0 + 32 * mb, lane), df[ks], dp[mb]);
-                }
+            // S = K Q^T and dP = V dO^T: 16 products, step j = (mb, ks) = (j / 8, j % 8) reads a
+            // K row chunk and a V^T fragment (two transposed reads), one step ahead.
+            {
+                u32x4 fk[2];
+                u32x2_t fvl[2], fvu[2];
+                auto rd = [&](auto j_t) __attribute__((always_inline)) {
+                    constexpr int j = decltype(j_t)::value, mb = j / 8, ks = j % 8;
+                    constexpr int koff = stg * kStage + (ks >> 1) * (Q_BKV * 64) + (k0 + 32 * mb) * 64;
+                    constexpr int voff = stg * kStage + ((k0 + 32 * mb) >> 5) * (D * 64) + ks * 1024;
+                    fk[j % 2] = ds_read16<koff>(ks & 1 ? ak1 : ak0);
+                    fvl[j % 2] = tr_read<voff>(pv_lo);
+                    fvu[j % 2] = tr_read<voff>(pv_up);
+                };
+                s[0] = s[1] = dp[0] = dp[1] = f32x16{};
+                rd(std::integral_constant<int, 0>{});
+                static_for<16>([&](auto j_t) __attribute__((always_inline)) {
+                    constexpr int j = decltype(j_t)::value, mb = j / 8, ks = j % 8;
+                    if constexpr (j + 1 < 16) {
+                        rd(std::integral_constant<int, j + 1>{});
+                        lgkm_wait3<3>(fk[j % 2], fvl[j % 2], fvu[j % 2]);
+                    } else {
+                        lgkm_wait3<0>(fk[j % 2], fvl[j % 2], fvu[j % 2]);
+                    }
+                    s[mb] = mfma32x32x16(as_bf16x8(fk[j % 2]), qf[ks], s[mb]);
+                    dp[mb] = mfma32x32x16(join_frag(fvl[j % 2], fvu[j % 2]), df[ks], dp[mb]);
+                });
             }
             // Register i of block mb holds key t0 + k0 + 32 mb + 16 (i / 8) + 8 hi + i % 8.
             bf16x8 db_[4];
@@ -599,12 +635,35 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
                     }
                     db_[2 * mb + h] = pack8(de);
                 }
-#pragma unroll
-            for (int c = 0; c < 4; ++c)
-#pragma unroll
-                for (int m = 0; m < 4; ++m)
-                    dq[m] = mfma32x32x16(tr_frag<Q_BKV, false>(lk[stg], k0 + 16 * c, 32 * m, lane), db_[c], dq[m]);
-        }
+            // dQ += dS K: 16 products, product i = (c, m) = (i / 4, i % 4), each K^T fragment two
+            // transposed reads, two products ahead through three rotating fragments.
+            {
+                u32x2_t flo[3], fup[3];
+                auto issue_k = [&](auto i_t) __attribute__((always_inline)) {
+                    constexpr int i = decltype(i_t)::value, c = i / 4, m = i % 4;
+                    constexpr int off = stg * kStage + m * (Q_BKV * 64) + (k0 + 16 * c) * 64;
+                    flo[i % 3] = tr_read<off>(tk_lo);
+                    fup[i % 3] = tr_read<off>(tk_up);
+                };
+                issue_k(std::integral_constant<int, 0>{});
+                issue_k(std::integral_constant<int, 1>{});
+                static_for<16>([&](auto i_t) __attribute__((always_inline)) {
+                    constexpr int i = decltype(i_t)::value, c = i / 4, m = i % 4;
+                    if constexpr (i + 1 < 16) lgkm_wait2<2>(flo[i % 3], fup[i % 3]);
+                    else lgkm_wait2<0>(flo[i % 3], fup[i % 3]);
+                    if constexpr (i + 2 < 16) issue_k(std::integral_constant<int, i + 2>{});
+                    dq[m] = mfma32x32x16(join_frag(flo[i % 3], fup[i % 3]), db_[c], dq[m]);
+                });
+            }
+        };
+        half(std::integral_constant<int, 0>{});
+        half(std::integral_constant<int, 1>{});
+    };
+
+    issue(0, 0);
+    for (int t = 0; t < ntiles; t += 2) {
+        tile(t, std::integral_constant<int, 0>{});
+        if (t + 1 < ntiles) tile(t + 1, std::integral_constant<int, 1>{});
     }
 
     // Epilogue: lane column = query ql; register e of block m holds dim
