@@ -263,6 +263,7 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
     const int b = grp / A.g, kvh = grp - b * A.g;
     const int r = A.a / A.g;
     const int k0w = kb * KV_BK + 32 * wave;
+    const int k0u = __builtin_amdgcn_readfirstlane(k0w);   // the same value, held as wave-uniform
     const int key = k0w + l32;                 // the key whose column this lane holds
     const bool kvalid = key < A.S;
     const size_t plane = (size_t)b * A.g + kvh;
@@ -352,6 +353,10 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
             constexpr int RB = decltype(rb_t)::value;
             const int rb = RB;
             if (qb0 + 32 * rb + 31 < k0w) return;   // every query of the half precedes the wave's keys
+            // Wave-uniform: some entry of the half is masked (a query before one of the wave's
+            // keys, or past S).  Most halves lie wholly below the diagonal and skip the mask.
+            const int q_first = qb0 + 32 * rb;
+            const bool masked = !(q_first >= k0u + 31 && q_first + 31 < A.S);
             f32x16 s = f32x16{}, dp = f32x16{};
             // S = Q K^T and dP = dO V^T over 8 k steps; step ks reads a Q row chunk, a dO row
             // chunk and a V^T fragment (two transposed reads), one step ahead of its products.
@@ -392,12 +397,19 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
                 float pe[8], de[8];
 #pragma unroll
                 for (int k = 0; k < 8; ++k) {
-                    const int qi = qb0 + qo + k;
                     const float lse = k < 4 ? l0[k] : l1[k - 4], dd = k < 4 ? d0[k] : d1[k - 4];
-                    const bool vis = key <= qi && qi < A.S;
                     const float e = __builtin_amdgcn_exp2f(fmaf(s[8 * h + k], A.scale_log2, -lse));
-                    pe[k] = vis ? e : 0.f;
-                    de[k] = vis ? e * (dp[8 * h + k] - dd) : 0.f;
+                    pe[k] = e;
+                    de[k] = e * (dp[8 * h + k] - dd);
+                }
+                if (masked) {
+#pragma unroll
+                    for (int k = 0; k < 8; ++k) {
+                        const int qi = qb0 + qo + k;
+                        const bool vis = key <= qi && qi < A.S;
+                        pe[k] = vis ? pe[k] : 0.f;
+                        de[k] = vis ? de[k] : 0.f;
+                    }
                 }
                 pa[h] = pack8(pe);
                 da[h] = pack8(de);
@@ -523,6 +535,7 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
     const int b = rest / A.a, head = rest - b * A.a;
     const int kvh = head / (A.a / A.g);
     const int q0w = qt * Q_BQ + 32 * wave;
+    const int q0u = __builtin_amdgcn_readfirstlane(q0w);   // the same value, held as wave-uniform
     const int ql = q0w + l32;                           // the query of this lane's column
     const size_t ld = (size_t)A.a * D;
 
@@ -591,6 +604,9 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
             constexpr int HF = decltype(hf_t)::value;
             constexpr int k0 = 64 * HF;                     // first key of the half in the tile
             if (t0 + k0 > q0w + 31) return;                // no key of the half is visible
+            // Wave-uniform: some entry of the half is masked (a key after one of the wave's
+            // queries, or a query past S).  Halves wholly below the diagonal skip the mask.
+            const bool masked = !(t0 + k0 + 63 <= q0u && q0u + 31 < A.S);
             f32x16 s[2], dp[2];
             // S = K Q^T and dP = V dO^T: 16 products, step j = (mb, ks) = (j / 8, j % 8) reads a
             // K row chunk and a V^T fragment (two transposed reads), one step ahead.
@@ -628,10 +644,15 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
                     float de[8];
 #pragma unroll
                     for (int k = 0; k < 8; ++k) {
-                        const int kk = t0 + k0 + 32 * mb + 16 * h + 8 * hi + k;
-                        const bool vis = kk <= ql && ql < A.S;
                         const float e = __builtin_amdgcn_exp2f(fmaf(s[mb][8 * h + k], A.scale_log2, -lse));
-                        de[k] = vis ? e * (dp[mb][8 * h + k] - dd) : 0.f;
+                        de[k] = e * (dp[mb][8 * h + k] - dd);
+                    }
+                    if (masked) {
+#pragma unroll
+                        for (int k = 0; k < 8; ++k) {
+                            const int kk = t0 + k0 + 32 * mb + 16 * h + 8 * hi + k;
+                            de[k] = kk <= ql && ql < A.S ? de[k] : 0.f;
+                        }
                     }
                     db_[2 * mb + h] = pack8(de);
                 }
