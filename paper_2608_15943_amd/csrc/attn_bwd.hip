@@ -26,6 +26,11 @@
 // straight from registers.  Operands that run along a staged tile's rows (dO, Q and V^T
 // for dV, dK and dP; K and V^T in the dQ kernel) are read with the LDS transpose read of
 // gfx950, so every tile is staged once, in the layout it has in memory.
+//
+// Inside the loops the LDS fragment reads are placed by hand ahead of the products that
+// consume them (the compiled order waited for every fragment right before its MFMA), and
+// the causal mask is applied only in the blocks that touch the diagonal or the end of the
+// sequence, behind a wave-uniform branch; every other block computes P and dS unmasked.
 #include <math.h>
 
 #include <algorithm>
