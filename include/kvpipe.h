@@ -438,9 +438,10 @@ int kvp_pager_rows(const kvp_pager* p, const int32_t* seqs, int B, int32_t* out)
  * recompute it).  The producers' K/V slots hold what the forward wrote; the
  * backward reads them.  Layout: layer l's record starts at l * stride and holds,
  * in this order and each starting on a 256-byte boundary, Q_l, O_l, X_l (its
- * bytes are reserved, unwritten, for l = 0) and (bf16) the log-sum-exp;
- * stride = the record's size rounded up to 256 bytes, and the buffer is
- * L * stride bytes.  Callers may read these tensors after the forward (e.g. to
+ * bytes are reserved, unwritten, for l = 0), (bf16) the log-sum-exp, and (bf16,
+ * when B*S is a multiple of 512 and S a multiple of 8) O_l^T ([a*d_h, B*S], the
+ * values of O_l token-major, the operand of dW_O); stride = the record's size
+ * rounded up to 256 bytes, and the buffer is L * stride bytes.  Callers may read these tensors after the forward (e.g. to
  * check a layer against a reference fed the same X_l).
  *
  * The backward runs the layers last to first.  For layer l with producer

@@ -39,6 +39,7 @@
 #include "common.h"
 #include "kernels.h"
 #include "lds_tr.h"
+#include "tokmajor.h"
 
 namespace kvp {
 namespace {
@@ -248,6 +249,7 @@ struct KvArgs {
     float* acc_out_k;       // may alias acc_in_*
     float* acc_out_v;
     uint16_t* out;          // final rows [B*S][ldo] or null; dK at col_k + kvh*128, dV at col_v
+    uint16_t* out_t;        // null, or the same values token-major [ldo][B*S] (S % 8 == 0)
     int ldo, col_k, col_v;
     int B, S, Sp, a, g, cap;
     float scale_log2, scale;
@@ -458,6 +460,13 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
     // Epilogue: lane column d = 32 nb + l32; register e of block nb holds key
     // k0w + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate dK back (pairs nb, nb + 2), add the
     // consumers' shares, write.
+    // The token-major copy is staged per wave, dK in the V^T buffer and dV in the Q / dO
+    // stages (all free once every wave is past its last block): the lane's 4 consecutive
+    // keys of each dimension as one 8-byte LDS write.
+    uint32_t tk[4][2], tv[4][2];             // the group's 4 keys, packed in pairs
+    uint16_t* tsk = (uint16_t*)&lvt[0] + wave * (D * 32);
+    uint16_t* tsv = wave < 4 ? (uint16_t*)&lq[0][0] + wave * (D * 32) : (uint16_t*)&ldo_[0][0] + (wave - 4) * (D * 32);
+    if (A.out_t) __syncthreads();
 #pragma unroll
     for (int e = 0; e < 16; ++e) {
         const int kk = k0w + 8 * (e >> 2) + 4 * hi + (e & 3);
@@ -491,14 +500,28 @@ __global__ __launch_bounds__(KV_NT, 2) void flash_bwd_kv_kernel(KvArgs A) {
                 uint16_t* row = A.out + ((size_t)b * A.S + kk) * A.ldo + kvh * D + l32;
 #pragma unroll
                 for (int nb = 0; nb < 4; ++nb) {
-                    row[A.col_k + 32 * nb] = f2bf(yk[nb]);
-                    row[A.col_v + 32 * nb] = f2bf(yv[nb]);
+                    const uint16_t bk = f2bf(yk[nb]), bv = f2bf(yv[nb]);
+                    row[A.col_k + 32 * nb] = bk;
+                    row[A.col_v + 32 * nb] = bv;
+                    const int sh = 16 * (e & 1), ix = (e >> 1) & 1;
+                    tk[nb][ix] = (e & 1) ? (tk[nb][ix] | ((uint32_t)bk << sh)) : (uint32_t)bk;
+                    tv[nb][ix] = (e & 1) ? (tv[nb][ix] | ((uint32_t)bv << sh)) : (uint32_t)bv;
                 }
             }
-        } else {
-#pragma unroll
-            for (int nb = 0; nb < 4; ++nb) yk[nb] = yv[nb] = 0.f;
         }
+        if ((e & 3) == 3 && A.out_t) {
+            const int k4 = 8 * (e >> 2) + 4 * hi;    // the group's first key within the wave's 32
+#pragma unroll
+            for (int nb = 0; nb < 4; ++nb) {
+                tm_put_dim(tsk, 32 * nb + l32, k4, u32x2{tk[nb][0], tk[nb][1]});
+                tm_put_dim(tsv, 32 * nb + l32, k4, u32x2{tv[nb][0], tv[nb][1]});
+            }
+        }
+    }
+    if (A.out_t) {
+        const size_t ldt = (size_t)A.B * A.S, t0 = (size_t)b * A.S + k0w;
+        tm_flush(tsk, A.out_t, ldt, A.col_k + kvh * D, t0, A.S - k0w, lane);
+        tm_flush(tsv, A.out_t, ldt, A.col_v + kvh * D, t0, A.S - k0w, lane);
     }
 }
 
@@ -520,6 +543,7 @@ struct QArgs {
     const uint16_t* vc;     // producer V slot [Bmax][g][128][cap]
     const float2* rope;     // [S][64]
     uint16_t* out;          // dQ rows [B*S][ldo] at column head*128
+    uint16_t* out_t;        // null, or dQ token-major [ldo][B*S] (S % 8 == 0)
     int ldo;
     int B, S, Sp, a, g, cap;
     float scale_log2, scale;
@@ -693,7 +717,11 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
     }
 
     // Epilogue: lane column = query ql; register e of block m holds dim
-    // 32 m + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate back (pairs m, m + 2), write.
+    // 32 m + 8 (e / 4) + 4 hi + e % 4.  Scale, rotate back (pairs m, m + 2), write.  The
+    // token-major copy is staged per wave in the K buffers (free once every wave is past
+    // its last tile).
+    uint16_t* ts = (uint16_t*)&lk[0][0] + wave * (D * 32);
+    if (A.out_t) __syncthreads();
     if (ql < A.S) {
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
@@ -716,9 +744,12 @@ __global__ __launch_bounds__(Q_NT, 2) void flash_bwd_q_kernel(QArgs A) {
                 w[0] = pack2bf(y[m][0], y[m][1]);
                 w[1] = pack2bf(y[m][2], y[m][3]);
                 *(u32x2*)(A.out + ((size_t)b * A.S + ql) * A.ldo + head * D + d0) = w;
+                if (A.out_t) tm_put_token(ts, d0, l32, w);
             }
         }
     }
+    if (A.out_t)
+        tm_flush(ts, A.out_t, (size_t)A.B * A.S, head * D, (size_t)b * A.S + q0w, A.S - q0w, lane);
 }
 
 }  // namespace
@@ -764,7 +795,8 @@ hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
     KvArgs A;
     A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.vc = p.vc; A.rope = p.rope;
     A.acc_in_k = p.acc_in_k; A.acc_in_v = p.acc_in_v; A.acc_out_k = p.acc_out_k; A.acc_out_v = p.acc_out_v;
-    A.out = p.out; A.ldo = p.ldo; A.col_k = p.col_k; A.col_v = p.col_v;
+    A.out = p.out; A.out_t = p.out_t; A.ldo = p.ldo; A.col_k = p.col_k; A.col_v = p.col_v;
+    if (p.out_t && (!p.out || p.S % 8 != 0)) return hipErrorInvalidValue;
     A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
@@ -776,7 +808,8 @@ hipError_t flash_bwd_kv_bf16(const AttnBwdKv& p, hipStream_t st) {
 hipError_t flash_bwd_q_bf16(const AttnBwdQ& p, hipStream_t st) {
     QArgs A;
     A.q = p.q; A.dO = p.dO; A.lse = p.lse; A.dsum = p.dsum; A.kc = p.kc; A.vc = p.vc;
-    A.rope = p.rope; A.out = p.out; A.ldo = p.ldo;
+    A.rope = p.rope; A.out = p.out; A.out_t = p.out_t; A.ldo = p.ldo;
+    if (p.out_t && p.S % 8 != 0) return hipErrorInvalidValue;
     A.B = p.B; A.S = p.S; A.Sp = p.Sp; A.a = p.a; A.g = p.g; A.cap = p.cap;
     A.scale = (float)(1.0 / sqrt((double)D));
     A.scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));

@@ -49,6 +49,7 @@
 
 #include "common.h"
 #include "kernels.h"
+#include "tokmajor.h"
 
 namespace kvp {
 namespace {
@@ -93,8 +94,8 @@ __device__ __forceinline__ void lgkm_wait(u32x4 (&f)[4]) {
 template <bool PAGED>
 __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     const uint16_t* __restrict__ Q, const uint16_t* __restrict__ Kc, const uint16_t* __restrict__ Vc,
-    uint16_t* __restrict__ O, float* __restrict__ lse, int Sp, int B, int S, int a, int g, int cap,
-    float scale_log2, Pages pages) {
+    uint16_t* __restrict__ O, float* __restrict__ lse, uint16_t* __restrict__ Ot, int Sp, int B, int S, int a,
+    int g, int cap, float scale_log2, Pages pages) {
     // K: [stage][row * 16 + (chunk ^ (row & 15))]; V^T: [stage][d * 16 + (chunk ^ (d & 15))]
     // (rows of 256 bytes: 128 dims of a position, or 128 positions of a dim).
     __shared__ u32x4 lk[2][BKV * 16];
@@ -405,7 +406,11 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
     }
 
     // ---- normalise and store O[b, q, head, :] -------------------------------------
-    // Lanes q and q ^ 32 hold the same query, so both take this branch or neither.
+    // Lanes q and q ^ 32 hold the same query, so both take this branch or neither.  The
+    // token-major copy (training) is staged in the K buffers, free once every wave is past
+    // its last tile.
+    uint16_t* ts = (uint16_t*)&lk[0][0] + wave * (D * 32);
+    if (Ot) __syncthreads();
     if (q_lane < S) {
         const float l_tot = pair32_sum(l_run);
         const float inv = 1.0f / l_tot;
@@ -420,24 +425,27 @@ __global__ __launch_bounds__(NT, 2) void flash_prefill_kernel(
                 w[0] = pack2bf(o[db][4 * r4 + 0] * inv, o[db][4 * r4 + 1] * inv);
                 w[1] = pack2bf(o[db][4 * r4 + 2] * inv, o[db][4 * r4 + 3] * inv);
                 *(u32x2*)(orow + d0) = w;
+                if (Ot) tm_put_token(ts, d0, l32, w);
             }
     }
+    if (Ot) tm_flush(ts, Ot, (size_t)B * S, head * D, (size_t)b * S + q0w, S - q0w, lane);
 }
 
 }  // namespace
 
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                              uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
-                              const Pages& pages, hipStream_t st) {
+                              uint16_t* o, float* lse, uint16_t* ot, int Sp, int B, int S, int a, int g,
+                              int cap, const Pages& pages, hipStream_t st) {
+    if (ot && (pages.pt || S % 8 != 0)) return hipErrorInvalidValue;
     const int nqt = (S + BQ - 1) / BQ;
     const float scale_log2 = (float)(1.4426950408889634 / sqrt((double)D));
     if (pages.pt) {
         if (pages.n < 1 || pages.stride < 1 || S > kPage * pages.stride) return hipErrorInvalidValue;
         hipLaunchKernelGGL(flash_prefill_kernel<true>, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, lse,
-                           Sp, B, S, a, g, cap, scale_log2, pages);
+                           nullptr, Sp, B, S, a, g, cap, scale_log2, pages);
     } else {
         hipLaunchKernelGGL(flash_prefill_kernel<false>, dim3(nqt * a * B), dim3(NT), 0, st, q, kc, vc, o, lse,
-                           Sp, B, S, a, g, cap, scale_log2, pages);
+                           ot, Sp, B, S, a, g, cap, scale_log2, pages);
     }
     return hipGetLastError();
 }

@@ -51,9 +51,11 @@ hipError_t gemm_resid_bf16(const uint16_t* a, const uint16_t* w, const void* x_r
 // Causal flash attention: q [B*S][a*128], K/V slots (or pools, pages.pt set) of the
 // producer, o [B*S][a*128]; lse (optional) [B][a][Sp]: the row log-sum-exp of the scaled
 // scores, log2 domain.
+// ot (nullable): a token-major copy O^T [a*128][B*S] of the same bf16 values (the backward's
+// dW_O operand); slots only, and S % 8 == 0.
 hipError_t flash_prefill_bf16(const uint16_t* q, const uint16_t* kc, const uint16_t* vc,
-                              uint16_t* o, float* lse, int Sp, int B, int S, int a, int g, int cap,
-                              const Pages& pages, hipStream_t st);
+                              uint16_t* o, float* lse, uint16_t* ot, int Sp, int B, int S, int a, int g,
+                              int cap, const Pages& pages, hipStream_t st);
 
 // The slice count gemm_kmajor_out_bf16 should use for an M x N x K product.
 int gemm_out_splits(int M, int N, int K);
@@ -97,6 +99,7 @@ struct AttnBwdKv {
     float* acc_out_k;
     float* acc_out_v;
     uint16_t* out;
+    uint16_t* out_t;        // nullable: the same rows token-major, [ldo][B*S] (S % 8 == 0)
     int ldo, col_k, col_v;
     int B, S, Sp, a, g, cap;
 };
@@ -111,6 +114,7 @@ struct AttnBwdQ {
     const uint16_t* vc;
     const float2* rope;
     uint16_t* out;
+    uint16_t* out_t;        // nullable: dQ token-major, [ldo][B*S] rows head*128 + d (S % 8 == 0)
     int ldo;
     int B, S, Sp, a, g, cap;
 };

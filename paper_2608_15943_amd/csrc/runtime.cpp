@@ -271,7 +271,7 @@ kvp::WRows proj_rows(const kvp_ctx* c, int l, bool producer) {
 // (and io.yf), attention output into o_buf.
 int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* ws,
                       const Workspace& w, int B, int S, hipStream_t st, void* q_buf = nullptr,
-                      float* lse = nullptr, const PageTable* pt = nullptr) {
+                      float* lse = nullptr, const PageTable* pt = nullptr, void* ot = nullptr) {
     const int p = c->tau[l];
     const bool producer = p == l;
     const Layer& P = c->layers[p];
@@ -303,8 +303,8 @@ int run_prefill_layer(kvp_ctx* c, int l, const LayerIO& io, void* o_buf, char* w
         if ((rc = timed(c, KVP_K_FLASH_ATTN, st, [&] {
                  return check_hip(kvp::flash_prefill_bf16(qo.q, (const uint16_t*)kv.k,
                                                           (const uint16_t*)kv.v, (uint16_t*)o_buf, lse,
-                                                          (S + 63) / 64 * 64, B, S, c->d.a, c->d.g,
-                                                          kv.cap, kv.pages, st),
+                                                          (uint16_t*)ot, (S + 63) / 64 * 64, B, S, c->d.a,
+                                                          c->d.g, kv.cap, kv.pages, st),
                                   "flash attention");
              })))
             return rc;
@@ -623,12 +623,17 @@ int round64(int S) { return (S + 63) / 64 * 64; }
 // Token counts that are multiples of this take the row-major weight-gradient GEMMs on
 // transposed activations (64-wide K tiles times up to 8 split-K slices).
 constexpr int kTokGrain = 512;
+// On that path, when S % 8 == 0, the attention kernels write O^T and [dQ|dK|dV]^T
+// themselves (8-byte aligned token runs) instead of separate transposes.
+bool tokmajor_direct(int B, int S) { return (size_t)B * S % kTokGrain == 0 && S % 8 == 0; }
 
 // Per-layer activations of kvp_train_forward, layer l at l * stride: Q (after RoPE), the
 // attention output O and the layer input X in the model dtype, and (bf16 models) the
-// log-sum-exp of the scores, which fp32 models recompute.
+// log-sum-exp of the scores, which fp32 models recompute.  When the backward takes the
+// token-major weight-gradient path, the attention kernel also saves O^T [a*d_h][B*S].
 struct Saved {
-    size_t q = 0, o = 0, x = 0, lse = 0, stride = 0, total = 0;
+    size_t q = 0, o = 0, x = 0, lse = 0, ot = 0, stride = 0, total = 0;
+    bool has_ot = false;
 };
 
 Saved saved_layout(const kvp_ctx& c, int B, int S) {
@@ -644,6 +649,8 @@ Saved saved_layout(const kvp_ctx& c, int B, int S) {
     v.o = take(M * c.n_q() * e);
     v.x = take(M * c.d.h * e);
     if (c.bf16()) v.lse = take((size_t)B * c.d.a * round64(S) * sizeof(float));
+    v.has_ot = c.bf16() && tokmajor_direct(B, S);
+    if (v.has_ot) v.ot = take(M * c.n_q() * e);
     v.stride = off;
     v.total = off * c.d.L;
     return v;
@@ -957,7 +964,8 @@ extern "C" int kvp_train_forward(kvp_ctx* ctx, const void* x, void* y, int B, in
         }
         io.y = next_x;
         if ((rc = run_prefill_layer(ctx, l, io, lay + sv.o, base, w, B, S, st, lay + sv.q,
-                                    bf ? (float*)(lay + sv.lse) : nullptr)))
+                                    bf ? (float*)(lay + sv.lse) : nullptr, nullptr,
+                                    sv.has_ot ? lay + sv.ot : nullptr)))
             return rc;
     }
     return ok();
@@ -1162,14 +1170,16 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
         {
             const int s = kvp::gemm_out_splits(h, nq, M);
             if (nt) {
-                // dW_O = G^T O on the token-major copies (row-major GEMM, split K).
+                // dW_O = G^T O on the token-major copies (row-major GEMM, split K); O^T was
+                // saved by the forward's attention kernel when S % 8 == 0.
+                const uint16_t* Ot = sv.has_ot ? (const uint16_t*)(lay + sv.ot) : tb;
                 if ((rc = aux([&] {
                          int r2 = check_hip(kvp::transpose_bf16(gb, ta, M, h, h, M, st), "transpose G");
-                         if (!r2) r2 = check_hip(kvp::transpose_bf16(Ol, tb, M, nq, nq, M, st), "transpose O");
+                         if (!r2 && !sv.has_ot) r2 = check_hip(kvp::transpose_bf16(Ol, tb, M, nq, nq, M, st), "transpose O");
                          return r2;
                      })))
                     return rc;
-                if ((rc = gemm([&] { return check_hip(kvp::gemm_nt_out_splits(ta, tb, h, nq, M, s, part, st), "dW_O GEMM"); })))
+                if ((rc = gemm([&] { return check_hip(kvp::gemm_nt_out_splits(ta, Ot, h, nq, M, s, part, st), "dW_O GEMM"); })))
                     return rc;
             } else if ((rc = gemm([&] { return check_hip(kvp::gemm_kmajor_out_bf16(gb, h, Ol, nq, h, nq, M, s, part, st), "dW_O GEMM"); })))
                 return rc;
@@ -1196,6 +1206,7 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
                 a.acc_in_k = acc_written[l] ? ak : nullptr;
                 a.acc_in_v = acc_written[l] ? av : nullptr;
                 a.out = dqkv;
+                a.out_t = sv.has_ot ? ta : nullptr;   // [dQ|dK|dV]^T for dW_QKV (ta is free after dW_O)
                 a.ldo = np;
                 a.col_k = nq;
                 a.col_v = nq + nkv;
@@ -1210,6 +1221,7 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
             kvp::AttnBwdQ a{};
             a.q = Ql; a.dO = dO; a.lse = lse; a.dsum = dsum; a.kc = (const uint16_t*)Pl.kc;
             a.vc = (const uint16_t*)Pl.vc; a.rope = rope; a.out = dqkv; a.ldo = np;
+            a.out_t = sv.has_ot ? ta : nullptr;
             a.B = B; a.S = S; a.Sp = Sp; a.a = ctx->d.a; a.g = ctx->d.g; a.cap = ctx->d.kv_capacity;
             if ((rc = timed(ctx, KVP_K_BWD_ATTN_Q, st, [&] {
                      return check_hip(kvp::flash_bwd_q_bf16(a, st), "attention backward dQ");
@@ -1221,7 +1233,8 @@ extern "C" int kvp_backward(kvp_ctx* ctx, const void* x, const void* dy, void* d
             const int s = kvp::gemm_out_splits(np, h, M);
             if (nt) {
                 if ((rc = aux([&] {
-                         int r2 = check_hip(kvp::transpose_bf16(dqkv, ta, M, np, np, M, st), "transpose dQKV");
+                         int r2 = sv.has_ot ? 0 : check_hip(kvp::transpose_bf16(dqkv, ta, M, np, np, M, st),
+                                                            "transpose dQKV");
                          if (!r2) r2 = check_hip(kvp::transpose_bf16(Xl, tb, M, h, h, M, st), "transpose X");
                          return r2;
                      })))

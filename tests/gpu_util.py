@@ -132,20 +132,26 @@ def _align256(n: int) -> int:
 def saved_views(w: ki.Workload, saved: torch.Tensor, B: int, S: int):
     """Per-layer views of kvp_train_forward's `saved` buffer (bf16 models), in the layout
     the C ABI documents: layer l at l * stride holds Q [B*S, a*d_h], O [B*S, a*d_h], the
-    layer input X [B*S, h] (l >= 1) and the row log-sum-exp [B, a, S rounded up to 64]."""
+    layer input X [B*S, h] (l >= 1), the row log-sum-exp [B, a, S rounded up to 64] and,
+    when B*S % 512 == 0 and S % 8 == 0, O^T [a*d_h, B*S] (key "ot")."""
     M, nq = B * S, w.a * w.d_h
     q_off = 0
     o_off = q_off + _align256(M * nq * 2)
     x_off = o_off + _align256(M * nq * 2)
     lse_off = x_off + _align256(M * w.h * 2)
-    stride = lse_off + _align256(B * w.a * ((S + 63) // 64 * 64) * 4)
+    ot_off = lse_off + _align256(B * w.a * ((S + 63) // 64 * 64) * 4)
+    has_ot = M % 512 == 0 and S % 8 == 0
+    stride = ot_off + (_align256(M * nq * 2) if has_ot else 0)
     assert stride * w.L == saved.numel(), (stride * w.L, saved.numel())
     out = []
     for l in range(w.L):
         base = l * stride
-        out.append({
+        v = {
             "q": saved[base + q_off: base + q_off + M * nq * 2].view(torch.bfloat16).view(B, S, nq),
             "o": saved[base + o_off: base + o_off + M * nq * 2].view(torch.bfloat16).view(B, S, nq),
             "x": saved[base + x_off: base + x_off + M * w.h * 2].view(torch.bfloat16).view(B, S, w.h),
-        })
+        }
+        if has_ot:
+            v["ot"] = saved[base + ot_off: base + ot_off + M * nq * 2].view(torch.bfloat16).view(nq, M)
+        out.append(v)
     return out

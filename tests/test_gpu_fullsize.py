@@ -172,6 +172,10 @@ def test_prefill_70b_stage_composed_teacher_forced():
     assert torch.equal(y, y2), "kvp_train_forward and kvp_prefill differ"
     del y2
     sv = saved_views(w, saved, B, S)
+    # The attention kernel's token-major copy of O (the backward's dW_O operand) holds the
+    # same bf16 values as O itself.
+    for l in range(w.L):
+        assert torch.equal(sv[l]["ot"], sv[l]["o"].reshape(B * S, -1).t()), f"O^T of layer {l}"
     K0, V0 = dm.slots[0]
     k_gpu = to_np(K0[0, :, :S])                          # [g, S, d_h]
     v_gpu = to_np(V0[0, :, :, :S]).transpose(0, 2, 1)
