@@ -116,6 +116,11 @@ def _train_case(w, B, S, cap):
     (256, 2, 1, [0, 0], 2, 1),               # S = 1
     (256, 2, 1, [0, 0, 2], 2, 256),          # 512 tokens: weight gradients on token-major copies
     (1024, 8, 1, [0, 0], 1, 160),            # r = 8 (the 70B-shaped ratio), one consumer
+    # Token counts that are multiples of 512 with S % 8 == 0: the attention kernels write O^T
+    # and [dQ|dK|dV]^T themselves; S below a 32-token wave block (8), and one full block plus
+    # an 8-token tail (40), take the partial-run stores.
+    (256, 2, 1, [0, 0], 64, 8),
+    (256, 2, 1, [0, 0, 2], 64, 40),
 ])
 def test_backward_matches_oracle(h, a, g, tau, B, S):
     w = small_workload(f"bwd-h{h}-a{a}-g{g}", len(tau), h, a, g, tau, seed=21)
